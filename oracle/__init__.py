@@ -1,0 +1,165 @@
+"""fp64 CPU oracle for the SS2D selective-scan path (ctypes over ``oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg, never by the product path. It shares no code with
+the HIP kernels; see ``oracle.c`` for what each function computes and which
+passage of the paper it follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` with gcc (fp64, no FP contraction, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+               "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build(force=False)
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    scan_args = [P, P, P, P, P, P, P, ctypes.c_int, I64, I64, I64, I64, I64, P, I64, P, ctypes.c_int]
+    lib.oracle_full_scan.argtypes = scan_args
+    lib.oracle_full_scan.restype = None
+    lib.oracle_mean_scan.argtypes = scan_args
+    lib.oracle_mean_scan.restype = None
+    lib.oracle_cross_scan.argtypes = [P, P, I64, I64, I64, I64, I64]
+    lib.oracle_cross_merge_f64.argtypes = [P, P, I64, I64, I64, I64]
+    lib.oracle_cross_merge_f32.argtypes = [P, P, I64, I64, I64, I64]
+    lib.oracle_cross_merge_bf16.argtypes = [P, P, I64, I64, I64, I64]
+    lib.oracle_f32_to_bf16.argtypes = [P, P, I64]
+    lib.oracle_max_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _f32(a: Optional[np.ndarray]) -> Optional[np.ndarray]:
+    if a is None:
+        return None
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def _scan(fn_name, per_seq, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads):
+    lib = _load()
+    u, delta, A, B, C = map(_f32, (u, delta, A, B, C))
+    D, dt_bias = _f32(D), _f32(dt_bias)
+    batch, K, Dc, L = u.shape
+    N = A.shape[1]
+    assert delta.shape == u.shape and A.shape == (K * Dc, N)
+    assert B.shape == (batch, K, N, L) and C.shape == B.shape
+    if sel is None:
+        sel_arr = None
+        nsel = batch * K * (Dc if per_seq else 1)
+    else:
+        sel_arr = np.ascontiguousarray(np.asarray(sel, dtype=np.int64))
+        nsel = int(sel_arr.size)
+    shape = (nsel, L) if per_seq else (nsel, Dc, L)
+    y = np.empty(shape, dtype=np.float64)
+    getattr(lib, fn_name)(_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(dt_bias),
+                          int(bool(softplus)), batch, K, Dc, L, N, _ptr(sel_arr), nsel, _ptr(y),
+                          int(nthreads))
+    return y
+
+
+def full_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
+              sel: Optional[Sequence[int]] = None, nthreads: int = 0) -> np.ndarray:
+    """Full selective scan in fp64.
+
+    u, delta: [batch, K, Dc, L]; A: [K*Dc, N]; B, C: [batch, K, N, L];
+    D, dt_bias: [K*Dc] or None. Returns [batch, K, Dc, L] (sel None) or
+    [len(sel), L] for the flat sequence indices (b*K + k)*Dc + d in ``sel``.
+    """
+    y = _scan("oracle_full_scan", True, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads)
+    if sel is None:
+        return y.reshape(np.shape(u))
+    return y
+
+
+def mean_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
+              sel: Optional[Sequence[int]] = None, nthreads: int = 0) -> np.ndarray:
+    """VMeanba channel-mean scan in fp64, output broadcast over channels.
+
+    Returns [batch, K, Dc, L] (sel None) or [len(sel), Dc, L] for the flat
+    direction indices b*K + k in ``sel``.
+    """
+    y = _scan("oracle_mean_scan", False, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads)
+    if sel is None:
+        return y.reshape(np.shape(u))
+    return y
+
+
+def cross_scan(x: np.ndarray) -> np.ndarray:
+    """x [batch, Dc, H, W] -> [batch, 4, Dc, H*W] (any element type)."""
+    lib = _load()
+    x = np.ascontiguousarray(x)
+    batch, Dc, H, W = x.shape
+    xs = np.empty((batch, 4, Dc, H * W), dtype=x.dtype)
+    lib.oracle_cross_scan(_ptr(x), _ptr(xs), batch, Dc, H, W, x.dtype.itemsize)
+    return xs
+
+
+def cross_merge(ys: np.ndarray, H: int, W: int, precision: str = "f64") -> np.ndarray:
+    """ys [batch, 4, Dc, H*W] -> [batch, Dc, H, W].
+
+    precision "f64": double sums; "f32": binary32 sums in the fixed
+    association; "bf16": ys given as uint16 bfloat16 patterns, binary32 sums,
+    one nearest-even rounding (returns uint16 patterns).
+    """
+    lib = _load()
+    batch, K, Dc, L = ys.shape
+    assert K == 4 and L == H * W
+    if precision == "f64":
+        ys = np.ascontiguousarray(ys, dtype=np.float64)
+        y = np.empty((batch, Dc, H, W), dtype=np.float64)
+        lib.oracle_cross_merge_f64(_ptr(ys), _ptr(y), batch, Dc, H, W)
+    elif precision == "f32":
+        ys = np.ascontiguousarray(ys, dtype=np.float32)
+        y = np.empty((batch, Dc, H, W), dtype=np.float32)
+        lib.oracle_cross_merge_f32(_ptr(ys), _ptr(y), batch, Dc, H, W)
+    elif precision == "bf16":
+        ys = np.ascontiguousarray(ys, dtype=np.uint16)
+        y = np.empty((batch, Dc, H, W), dtype=np.uint16)
+        lib.oracle_cross_merge_bf16(_ptr(ys), _ptr(y), batch, Dc, H, W)
+    else:
+        raise ValueError(precision)
+    return y
+
+
+def to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """binary32 -> bfloat16 bit patterns, nearest-even (a bf16 store)."""
+    lib = _load()
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    out = np.empty(a.shape, dtype=np.uint16)
+    lib.oracle_f32_to_bf16(_ptr(a), _ptr(out), a.size)
+    return out

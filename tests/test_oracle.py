@@ -1,0 +1,422 @@
+"""Pins for the fp64 oracle: each test checks it against something other than
+itself -- a hand-worked example, a closed form, a library routine, or an
+invariant the method implies. CPU only."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.signal
+
+import oracle
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rand_case(seed, batch=1, K=2, Dc=3, L=9, N=3, softplus=True, with_d=True, with_bias=True):
+    rng = np.random.default_rng(seed)
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    u = f(batch, K, Dc, L)
+    delta = (0.5 * f(batch, K, Dc, L)).astype(np.float32)
+    A = (-rng.uniform(0.2, 2.0, size=(K * Dc, N))).astype(np.float32)
+    B = f(batch, K, N, L)
+    C = f(batch, K, N, L)
+    D = f(K * Dc) if with_d else None
+    bias = (0.3 * f(K * Dc)).astype(np.float32) if with_bias else None
+    return dict(u=u, delta=delta, A=A, B=B, C=C, D=D, dt_bias=bias, softplus=softplus)
+
+
+def timescale_np(delta, bias, softplus, K, Dc):
+    """Delta = softplus(delta + bias) with numpy's logaddexp as the softplus."""
+    v = delta.astype(np.float64)
+    if bias is not None:
+        v = v + bias.astype(np.float64).reshape(1, K, Dc, 1)
+    return np.logaddexp(0.0, v) if softplus else v
+
+
+def closed_form_full(c):
+    """Cumulative-product closed form of eq. 3 (no recurrence):
+    h[n,t] = sum_{s<=t} exp(A_n * sum_{r=s+1..t} Delta_r) * Delta_s * B[n,s] * u_s."""
+    u, A, B, C = c["u"], c["A"], c["B"], c["C"]
+    batch, K, Dc, L = u.shape
+    N = A.shape[1]
+    dl = timescale_np(c["delta"], c["dt_bias"], c["softplus"], K, Dc)
+    y = np.zeros((batch, K, Dc, L))
+    for b in range(batch):
+        for k in range(K):
+            for d in range(Dc):
+                ch = k * Dc + d
+                for t in range(L):
+                    acc = 0.0
+                    for n in range(N):
+                        h = 0.0
+                        for s in range(t + 1):
+                            decay = math.exp(float(A[ch, n]) * float(np.sum(dl[b, k, d, s + 1:t + 1])))
+                            h += decay * dl[b, k, d, s] * float(B[b, k, n, s]) * float(u[b, k, d, s])
+                        acc += float(C[b, k, n, t]) * h
+                    dskip = 0.0 if c["D"] is None else float(c["D"][ch])
+                    y[b, k, d, t] = acc + dskip * float(u[b, k, d, t])
+    return y
+
+
+def run_full(c, **kw):
+    return oracle.full_scan(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"], c["dt_bias"],
+                            c["softplus"], **kw)
+
+
+def run_mean(c, **kw):
+    return oracle.mean_scan(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"], c["dt_bias"],
+                            c["softplus"], **kw)
+
+
+# ---------------------------------------------------------------- golden
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _golden_case(g):
+    i = g["inputs"]
+    a = lambda key: np.asarray(i[key], dtype=np.float32)
+    if "A_over_ln2" in i:
+        A = (np.asarray(i["A_over_ln2"], dtype=np.float64) * math.log(2.0)).astype(np.float32)
+    else:
+        A = a("A")
+    return dict(u=a("u"), delta=a("delta"), A=A, B=a("B"), C=a("C"), D=a("D"),
+                dt_bias=a("dt_bias"), softplus=g["softplus"])
+
+
+@pytest.mark.parametrize("name", ["hand_two_channel.json", "hand_softplus.json"])
+def test_golden_full(name):
+    g = _golden(name)
+    c = _golden_case(g)
+    np.testing.assert_allclose(run_full(c), np.asarray(g["expected_full"]), rtol=g["rtol"], atol=0)
+
+
+def test_golden_mean():
+    g = _golden("hand_two_channel.json")
+    c = _golden_case(g)
+    np.testing.assert_allclose(run_mean(c), np.asarray(g["expected_mean"]), rtol=g["rtol"], atol=0)
+
+
+# ---------------------------------------------------------------- P1 closed form
+
+@pytest.mark.parametrize("seed,softplus,with_d,with_bias,N", [
+    (0, True, True, True, 3), (1, False, True, False, 2), (2, True, False, True, 1),
+    (3, True, True, False, 4), (4, False, False, True, 3)])
+def test_full_matches_cumulative_product_closed_form(seed, softplus, with_d, with_bias, N):
+    c = rand_case(seed, batch=2, K=2, Dc=2, L=8, N=N, softplus=softplus, with_d=with_d,
+                  with_bias=with_bias)
+    np.testing.assert_allclose(run_full(c), closed_form_full(c), rtol=1e-10, atol=1e-12)
+
+
+# ---------------------------------------------------------------- P2 LTI forms
+
+def _lti_case(seed, L=40, N=3, Dc=2, const_u=False):
+    rng = np.random.default_rng(seed)
+    K = 1
+    u = rng.standard_normal((1, K, Dc, L)).astype(np.float32)
+    if const_u:
+        u[...] = u[..., :1]
+    delta = np.repeat(rng.uniform(0.05, 0.4, size=(1, K, Dc, 1)), L, axis=3).astype(np.float32)
+    A = (-rng.uniform(0.3, 1.5, size=(K * Dc, N))).astype(np.float32)
+    Bn = rng.standard_normal((N,)).astype(np.float32)
+    Cn = rng.standard_normal((N,)).astype(np.float32)
+    B = np.broadcast_to(Bn.reshape(1, 1, N, 1), (1, K, N, L)).copy()
+    C = np.broadcast_to(Cn.reshape(1, 1, N, 1), (1, K, N, L)).copy()
+    D = rng.standard_normal((K * Dc,)).astype(np.float32)
+    return dict(u=u, delta=delta, A=A, B=B, C=C, D=D, dt_bias=None, softplus=False), Bn, Cn
+
+
+def test_lti_equals_iir_filter_per_state():
+    """Time-invariant Delta, B, C: each state is the first-order IIR filter
+    h_t = a h_{t-1} + (Delta B) u_t, i.e. scipy.signal.lfilter([Delta B], [1, -a])."""
+    c, Bn, Cn = _lti_case(7)
+    y = run_full(c)
+    Dc, L, N = c["u"].shape[2], c["u"].shape[3], c["A"].shape[1]
+    for d in range(Dc):
+        dl = float(c["delta"][0, 0, d, 0])
+        u = c["u"][0, 0, d].astype(np.float64)
+        ref = float(c["D"][d]) * u
+        for n in range(N):
+            a = math.exp(dl * float(c["A"][d, n]))
+            ref = ref + float(Cn[n]) * scipy.signal.lfilter([dl * float(Bn[n])], [1.0, -a], u)
+        np.testing.assert_allclose(y[0, 0, d], ref, rtol=1e-11, atol=1e-12)
+
+
+def test_lti_equals_convolution_kernel():
+    """eq. 5: with time-invariant parameters y = u * Kbar + D u, where
+    Kbar_j = sum_n C_n Abar_n^j Bbar_n."""
+    c, Bn, Cn = _lti_case(8, L=30)
+    y = run_full(c)
+    Dc, L, N = c["u"].shape[2], c["u"].shape[3], c["A"].shape[1]
+    j = np.arange(L)
+    for d in range(Dc):
+        dl = float(c["delta"][0, 0, d, 0])
+        kbar = np.zeros(L)
+        for n in range(N):
+            a = math.exp(dl * float(c["A"][d, n]))
+            kbar += float(Cn[n]) * a ** j * dl * float(Bn[n])
+        u = c["u"][0, 0, d].astype(np.float64)
+        ref = np.convolve(u, kbar)[:L] + float(c["D"][d]) * u
+        np.testing.assert_allclose(y[0, 0, d], ref, rtol=1e-11, atol=1e-12)
+
+
+def test_constant_input_geometric_series():
+    """Constant u, Delta, B: h_t = Delta B u (1 - a^(t+1)) / (1 - a)."""
+    c, Bn, Cn = _lti_case(9, L=25, const_u=True)
+    c["D"] = None
+    y = run_full(c)
+    N = c["A"].shape[1]
+    t = np.arange(c["u"].shape[3])
+    for d in range(c["u"].shape[2]):
+        dl = float(c["delta"][0, 0, d, 0])
+        uu = float(c["u"][0, 0, d, 0])
+        ref = np.zeros_like(t, dtype=np.float64)
+        for n in range(N):
+            a = math.exp(dl * float(c["A"][d, n]))
+            ref += float(Cn[n]) * dl * float(Bn[n]) * uu * (1 - a ** (t + 1)) / (1 - a)
+        np.testing.assert_allclose(y[0, 0, d], ref, rtol=1e-11, atol=1e-12)
+
+
+# ---------------------------------------------------------------- P3 N = 1, superposition
+
+def test_states_superpose():
+    """The output is linear in the states: the N-state run equals the sum of
+    N one-state runs minus the N-1 extra copies of the skip term."""
+    c = rand_case(11, batch=1, K=2, Dc=3, L=12, N=4)
+    y = run_full(c)
+    acc = np.zeros_like(y)
+    N = c["A"].shape[1]
+    for n in range(N):
+        cn = dict(c)
+        cn["A"] = np.ascontiguousarray(c["A"][:, n:n + 1])
+        cn["B"] = np.ascontiguousarray(c["B"][:, :, n:n + 1])
+        cn["C"] = np.ascontiguousarray(c["C"][:, :, n:n + 1])
+        acc += run_full(cn)
+    skip = c["D"].reshape(1, 2, 3, 1).astype(np.float64) * c["u"].astype(np.float64)
+    np.testing.assert_allclose(y, acc - (N - 1) * skip, rtol=1e-11, atol=1e-12)
+
+
+def test_n1_scalar_recurrence_by_hand_loop():
+    c = rand_case(12, batch=1, K=1, Dc=1, L=15, N=1, with_bias=False)
+    y = run_full(c)[0, 0, 0]
+    dl = np.logaddexp(0.0, c["delta"][0, 0, 0].astype(np.float64))
+    a = np.exp(dl * float(c["A"][0, 0]))
+    # unrolled closed form for N = 1: h_t = sum_s (prod_{r=s+1..t} a_r) bu_s
+    bu = dl * c["B"][0, 0, 0].astype(np.float64) * c["u"][0, 0, 0].astype(np.float64)
+    for t in range(15):
+        h = sum(np.prod(a[s + 1:t + 1]) * bu[s] for s in range(t + 1))
+        ref = float(c["C"][0, 0, 0, t]) * h + float(c["D"][0]) * float(c["u"][0, 0, 0, t])
+        assert abs(y[t] - ref) <= 1e-12 * max(1.0, abs(ref))
+
+
+# ---------------------------------------------------------------- P4 / P5 mean variant
+
+def test_mean_equals_full_when_channels_identical():
+    """Identical channels within a direction: the channel mean of the
+    discretised inputs is each channel's own, so VMeanba = the full scan."""
+    c = rand_case(13, batch=2, K=2, Dc=4, L=11, N=3)
+    for key in ("u", "delta"):
+        c[key][...] = c[key][:, :, :1, :]
+    A = c["A"].reshape(2, 4, 3)
+    A[...] = A[:, :1, :]
+    for key in ("D", "dt_bias"):
+        v = c[key].reshape(2, 4)
+        v[...] = v[:, :1]
+    np.testing.assert_allclose(run_mean(c), run_full(c), rtol=1e-13, atol=1e-14)
+
+
+def test_mean_is_channel_mean_of_full_when_timescale_shared():
+    """If Delta and A do not vary over channels, the recurrence is linear in u,
+    so under T = mean of (Abar, Bbar u, D u) the reduced output is exactly the
+    channel mean of the full outputs, even with per-channel u and D."""
+    c = rand_case(14, batch=1, K=3, Dc=5, L=10, N=3)
+    c["delta"][...] = c["delta"][:, :, :1, :]
+    A = c["A"].reshape(3, 5, 3)
+    A[...] = A[:, :1, :]
+    v = c["dt_bias"].reshape(3, 5)
+    v[...] = v[:, :1]
+    ym = run_mean(c)
+    yf = run_full(c)
+    ref = np.broadcast_to(yf.mean(axis=2, keepdims=True), yf.shape)
+    np.testing.assert_allclose(ym, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_mean_single_channel_is_full():
+    c = rand_case(15, batch=1, K=2, Dc=1, L=9, N=2)
+    np.testing.assert_allclose(run_mean(c), run_full(c), rtol=1e-13, atol=1e-14)
+
+
+def test_mean_output_is_broadcast():
+    c = rand_case(16, batch=1, K=2, Dc=4, L=7, N=2)
+    y = run_mean(c)
+    assert np.all(y == y[:, :, :1, :])
+
+
+# ---------------------------------------------------------------- P6 permutations
+
+@pytest.mark.parametrize("H,W", [(1, 1), (1, 5), (4, 1), (3, 3), (4, 6), (7, 7)])
+def test_cross_scan_maps(H, W):
+    rng = np.random.default_rng(H * 10 + W)
+    x = rng.standard_normal((2, 3, H, W)).astype(np.float32)
+    xs = oracle.cross_scan(x)
+    assert xs.shape == (2, 4, 3, H * W)
+    np.testing.assert_array_equal(xs[:, 0], x.reshape(2, 3, H * W))
+    np.testing.assert_array_equal(xs[:, 1], np.swapaxes(x, 2, 3).reshape(2, 3, H * W))
+    np.testing.assert_array_equal(xs[:, 2], xs[:, 0, :, ::-1])
+    np.testing.assert_array_equal(xs[:, 3], xs[:, 1, :, ::-1])
+    # every direction is a bijection of the positions
+    idx = np.arange(H * W, dtype=np.int64).reshape(1, 1, H, W)
+    p = oracle.cross_scan(idx)
+    for k in range(4):
+        assert sorted(p[0, k, 0].tolist()) == list(range(H * W))
+
+
+@pytest.mark.parametrize("H,W", [(1, 1), (2, 5), (5, 3), (7, 7), (8, 16)])
+def test_merge_of_scan_is_four_times_exact(H, W):
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((2, 3, H, W)).astype(np.float32)
+    xs = oracle.cross_scan(x)
+    np.testing.assert_array_equal(oracle.cross_merge(xs, H, W, "f32"), 4 * x)
+    np.testing.assert_array_equal(oracle.cross_merge(xs.astype(np.float64), H, W, "f64"), 4 * x.astype(np.float64))
+    xb = workloads.bf16_round(x)[1]
+    yb = oracle.cross_merge(oracle.cross_scan(xb), H, W, "bf16")
+    widened = (yb.astype(np.uint32) << 16).view(np.float32)
+    np.testing.assert_array_equal(widened, 4 * workloads.bf16_round(x)[0])
+
+
+def test_merge_is_adjoint_of_scan():
+    """<cross_scan(x), ys> = <x, cross_merge(ys)>: the merge sums exactly the
+    positions the scan copied to."""
+    rng = np.random.default_rng(4)
+    H, W = 5, 6
+    x = rng.standard_normal((2, 3, H, W))
+    ys = rng.standard_normal((2, 4, 3, H * W))
+    lhs = float(np.sum(oracle.cross_scan(x) * ys))
+    rhs = float(np.sum(x * oracle.cross_merge(ys, H, W, "f64")))
+    assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs))
+
+
+def test_merge_association_f32():
+    """binary32 merge = (y0 + y2) + (y1 + y3) in single precision, checked
+    against numpy float32 adds on the scan-order gathered values."""
+    rng = np.random.default_rng(5)
+    H, W = 4, 5
+    ys = (rng.standard_normal((1, 4, 2, H * W)) * np.array([1, 1e4, 1e-4, 3e3]).reshape(1, 4, 1, 1)).astype(np.float32)
+    y = oracle.cross_merge(ys, H, W, "f32")
+    L = H * W
+    hh, ww = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    p0 = hh * W + ww
+    p1 = ww * H + hh
+    g = [ys[0, 0][:, p0], ys[0, 1][:, p1], ys[0, 2][:, L - 1 - p0], ys[0, 3][:, L - 1 - p1]]
+    ref = (g[0] + g[2]) + (g[1] + g[3])
+    np.testing.assert_array_equal(y[0], ref)
+
+
+def test_bf16_rounding_matches_torch():
+    import torch
+    rng = np.random.default_rng(6)
+    a = (rng.standard_normal(4096) * 10.0 ** rng.integers(-20, 20, 4096)).astype(np.float32)
+    a[:4] = [0.0, -0.0, np.inf, -np.inf]
+    ours = oracle.to_bf16_bits(a)
+    ref = torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(ours, ref)
+
+
+# ---------------------------------------------------------------- P7 combine algebra
+
+def _combine(p, q):
+    (a1, b1), (a2, b2) = p, q
+    return (a1 * a2, a2 * b1 + b2)
+
+
+def test_associative_combine_matches_sequential_scan():
+    """The (a, b) combine used by a parallel scan, applied over random
+    chunkings and tree orders, reproduces the oracle's sequential states."""
+    rng = np.random.default_rng(17)
+    L = 64
+    c = rand_case(17, batch=1, K=1, Dc=1, L=L, N=1, with_d=False)
+    c["C"][...] = 1.0
+    h_ref = run_full(c)[0, 0, 0]
+    dl = np.logaddexp(0.0, c["delta"][0, 0, 0].astype(np.float64) + float(c["dt_bias"][0]))
+    a = np.exp(dl * float(c["A"][0, 0]))
+    b = dl * c["B"][0, 0, 0].astype(np.float64) * c["u"][0, 0, 0].astype(np.float64)
+    for trial in range(20):
+        cuts = np.sort(rng.choice(np.arange(1, L), size=rng.integers(1, 12), replace=False))
+        chunks = np.split(np.arange(L), cuts)
+        aggs = []
+        for ch in chunks:  # chunk aggregate, combined in a random tree order
+            items = [(a[i], b[i]) for i in ch]
+            while len(items) > 1:
+                j = int(rng.integers(0, len(items) - 1))
+                items[j:j + 2] = [_combine(items[j], items[j + 1])]
+            aggs.append(items[0])
+        carry = (1.0, 0.0)
+        for ch, agg in zip(chunks, aggs):
+            h = carry[1]
+            for i in ch:
+                h = a[i] * h + b[i]
+                assert abs(h - h_ref[i]) <= 1e-12 * max(1.0, abs(h_ref[i]))
+            carry = _combine(carry, agg)
+            assert abs(carry[1] - h_ref[ch[-1]]) <= 1e-12 * max(1.0, abs(h_ref[ch[-1]]))
+
+
+# ---------------------------------------------------------------- P8 softplus / timescale
+
+def test_timescale_is_softplus_of_biased_delta():
+    """One step, A = 0, B = C = u = 1, D = 0: y = Delta = softplus(delta + bias)."""
+    v = np.concatenate([np.linspace(-30, 30, 61), [-80.0, 80.0, 1e-6, -1e-6]]).astype(np.float32)
+    n = v.size
+    u = np.ones((1, 1, n, 1), np.float32)
+    c = dict(u=u, delta=v.reshape(1, 1, n, 1), A=np.zeros((n, 1), np.float32),
+             B=np.ones((1, 1, 1, 1), np.float32), C=np.ones((1, 1, 1, 1), np.float32), D=None,
+             dt_bias=np.zeros(n, np.float32), softplus=True)
+    y = run_full(c)[0, 0, :, 0]
+    np.testing.assert_allclose(y, np.logaddexp(0.0, v.astype(np.float64)), rtol=1e-14, atol=0)
+    c["softplus"] = False
+    np.testing.assert_array_equal(run_full(c)[0, 0, :, 0], v.astype(np.float64))
+
+
+def test_dt_bias_inverts_softplus():
+    """The generator's dt_bias = softplus^-1(dt): with delta = 0 the oracle's
+    timescale is dt, log-uniform in [1e-3, 1e-1]."""
+    inp = workloads.make_inputs(workloads.TINY, "seq")
+    n = inp.dt_bias.size
+    c = dict(u=np.ones((1, 1, n, 1), np.float32), delta=np.zeros((1, 1, n, 1), np.float32),
+             A=np.zeros((n, 1), np.float32), B=np.ones((1, 1, 1, 1), np.float32),
+             C=np.ones((1, 1, 1, 1), np.float32), D=None, dt_bias=inp.dt_bias, softplus=True)
+    dt = run_full(c)[0, 0, :, 0]
+    assert dt.min() >= 1e-3 * (1 - 1e-5) and dt.max() <= 1e-1 * (1 + 1e-5)
+
+
+# ---------------------------------------------------------------- selection / threads
+
+def test_selected_sequences_match_full_output():
+    c = rand_case(18, batch=2, K=4, Dc=3, L=6, N=2)
+    y = run_full(c)
+    sel = [0, 5, 23, 11]
+    ys = run_full(c, sel=sel)
+    flat = y.reshape(-1, 6)
+    np.testing.assert_array_equal(ys, flat[sel])
+    ym = run_mean(c)
+    selm = [7, 2]
+    np.testing.assert_array_equal(run_mean(c, sel=selm), ym.reshape(8, 3, 6)[selm])
+
+
+def test_thread_count_does_not_change_results():
+    c = rand_case(19, batch=2, K=4, Dc=5, L=20, N=3)
+    np.testing.assert_array_equal(run_full(c, nthreads=1), run_full(c, nthreads=4))
+    np.testing.assert_array_equal(run_mean(c, nthreads=1), run_mean(c, nthreads=4))
+
+
+def test_degenerate_sizes():
+    c = rand_case(20, batch=1, K=1, Dc=1, L=1, N=1)
+    y = run_full(c)
+    dl = float(np.logaddexp(0.0, float(c["delta"].ravel()[0]) + float(c["dt_bias"][0])))
+    ref = float(c["C"].ravel()[0]) * dl * float(c["B"].ravel()[0]) * float(c["u"].ravel()[0]) \
+        + float(c["D"][0]) * float(c["u"].ravel()[0])
+    assert abs(y.ravel()[0] - ref) <= 1e-14 * max(1.0, abs(ref))
