@@ -1,0 +1,179 @@
+/*
+ * vmb.h -- C ABI of the MI355X (gfx950) SS2D selective-scan library (libvmb.so).
+ *
+ * The library implements the hot path of one SS2D block as described by
+ * VMeanba (arXiv 2412.16602), Appendix A (VMamba paragraph) and Section 2.2:
+ *
+ *   cross-scan  : unfold an H x W feature map into K = 4 sequences of length
+ *                 L = H*W (row-major, column-major and their reverses);
+ *   scan        : the Mamba selective scan of eq. 3 with Abar = exp(Delta*A)
+ *                 (eq. 4, first line), Bbar*u = Delta*B*u, and
+ *                 Delta = softplus(delta + dt_bias) (eq. 6) -- either per
+ *                 channel (full) or on the channel mean of the discretised
+ *                 inputs with the result broadcast back (VMeanba, eq. 9);
+ *   cross-merge : fold the four sequences back into one H x W map.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor arguments are DEVICE pointers to contiguous row-major
+ *    buffers owned by the caller. The library keeps no pointer after a call
+ *    returns and allocates no device memory; scratch space is passed in as
+ *    `workspace` (size from vmb_scan_workspace_bytes).
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL means the
+ *    null stream) and never synchronises. Calls on one stream run in order.
+ *  - Every argument is validated on the host BEFORE any device work is
+ *    enqueued; on a non-VMB_OK status nothing was launched and nothing was
+ *    written. No call prints, aborts or throws.
+ *  - Base pointers of streamed tensors (x, xs, ys, y, u, delta, B, C,
+ *    workspace) must be 16-byte aligned; A, D and dt_bias 4-byte aligned.
+ *  - Outputs must not overlap any input (VMB_ERR_ALIAS); in-place is not
+ *    supported.
+ *  - Non-finite inputs are not checked; they propagate.
+ *  - The library is stateless and thread-safe. Results are deterministic:
+ *    no floating-point atomics, fixed summation orders.
+ *  - Sizes are int64_t; a tensor may hold up to 2^31 - 1 elements per
+ *    [.., L] sequence row and 2^40 elements in total.
+ */
+#ifndef VMB_H
+#define VMB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VMB_ABI_VERSION 1
+
+typedef void* vmb_stream_t; /* a hipStream_t */
+
+typedef enum {
+    VMB_OK = 0,
+    VMB_ERR_NULL = 1,        /* a required pointer is NULL                         */
+    VMB_ERR_SHAPE = 2,       /* a size is < 1, inconsistent or too large           */
+    VMB_ERR_DTYPE = 3,       /* dtype value or dtype combination not supported     */
+    VMB_ERR_ALIGN = 4,       /* a base pointer violates the alignment rule         */
+    VMB_ERR_ALIAS = 5,       /* an output overlaps an input                        */
+    VMB_ERR_UNSUPPORTED = 6, /* valid but unsupported (e.g. N not in {1,2,4,8,16}) */
+    VMB_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than required            */
+    VMB_ERR_HIP = 8          /* the HIP runtime reported an error at launch        */
+} vmb_status;
+
+typedef enum {
+    VMB_F32 = 0,  /* IEEE binary32                                      */
+    VMB_BF16 = 1  /* bfloat16 (top half of binary32); stores round to nearest even */
+} vmb_dtype;
+
+typedef enum {
+    /* u, delta, y are per-direction sequences [batch, K, channels, L]. */
+    VMB_LAYOUT_SEQ = 0,
+    /* u is the feature map x [batch, channels, H, W], read through the
+     * cross-scan maps; y is the merged map [batch, channels, H, W].
+     * delta stays [batch, K, channels, L]. Requires K == 4 and L == H*W. */
+    VMB_LAYOUT_2D = 1
+} vmb_layout;
+
+/*
+ * Cross-scan (Appendix A, VMamba: "unfold the input feature map along four
+ * directions"). For pixel (h, w) of x[b, d] and L = H*W:
+ *   xs[b, 0, d, h*W + w]          = x[b, d, h, w]   (row-major)
+ *   xs[b, 1, d, w*H + h]          = x[b, d, h, w]   (column-major)
+ *   xs[b, 2, d, L - 1 - (h*W+w)]  = x[b, d, h, w]   (row-major, reversed)
+ *   xs[b, 3, d, L - 1 - (w*H+h)]  = x[b, d, h, w]   (column-major, reversed)
+ *
+ *   x  : [batch, channels, H, W] of dtype dt (input)
+ *   xs : [batch, 4, channels, H*W] of dtype dt (output)
+ * A pure copy: bit-exact for both dtypes.
+ */
+vmb_status vmb_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
+                          int64_t H, int64_t W, vmb_dtype dt, vmb_stream_t stream);
+
+/*
+ * Cross-merge (Appendix A, VMamba: "merges the 4 sets of 1D sequences back
+ * to 2D feature map"), the sum over directions at each pixel:
+ *   y[b, d, h, w] = (ys[b,0,d,pi_0] + ys[b,2,d,pi_2]) + (ys[b,1,d,pi_1] + ys[b,3,d,pi_3])
+ * with pi_k the positions listed for vmb_cross_scan, evaluated in binary32
+ * in exactly this association (bf16 inputs widened exactly, one
+ * nearest-even rounding at the end for a bf16 output).
+ *
+ *   ys : [batch, 4, channels, H*W] of dtype dt (input)
+ *   y  : [batch, channels, H, W] of dtype dt (output)
+ */
+vmb_status vmb_cross_merge(const void* ys, void* y, int64_t batch, int64_t channels,
+                           int64_t H, int64_t W, vmb_dtype dt, vmb_stream_t stream);
+
+/*
+ * Full selective scan (Appendix A: eq. 3, eq. 4 first line, eq. 6), one
+ * recurrence per (b, k, d, n), c = k*channels + d:
+ *   Delta_t = softplus(delta[b,k,d,t] + dt_bias[c])   (delta_softplus != 0)
+ *           = delta[b,k,d,t] + dt_bias[c]             (delta_softplus == 0)
+ *   h_{-1}  = 0
+ *   h_t[n]  = exp(Delta_t * A[c,n]) * h_{t-1}[n] + Delta_t * B[b,k,n,t] * u[b,k,d,t]
+ *   y_t     = sum_n C[b,k,n,t] * h_t[n] + D[c] * u[b,k,d,t]
+ * State and accumulation in binary32 for both input dtypes.
+ *
+ *   u        : in_dtype, [batch, K, channels, L] (SEQ) or x [batch, channels, H, W] (2D)
+ *   delta    : in_dtype, [batch, K, channels, L]
+ *   A        : float32,  [K*channels, N]  (negative for a decaying state)
+ *   B, C     : in_dtype, [batch, K, N, L]
+ *   D        : float32,  [K*channels] or NULL (treated as 0)
+ *   dt_bias  : float32,  [K*channels] or NULL (treated as 0)
+ *   y        : out_dtype, [batch, K, channels, L] (SEQ) or [batch, channels, H, W] (2D)
+ *   N        : 1, 2, 4, 8 or 16
+ *   (in_dtype, out_dtype) : (F32, F32), (BF16, BF16) or (BF16, F32)
+ *   H, W     : used by the 2D layout only (ignored for SEQ)
+ *   workspace: device scratch of at least vmb_scan_workspace_bytes(0, ...)
+ *              bytes (may be NULL when that is 0); contents on entry are
+ *              irrelevant and undefined on exit.
+ */
+vmb_status vmb_selective_scan_fwd(const void* u, const void* delta, const float* A,
+                                  const void* B, const void* C, const float* D,
+                                  const float* dt_bias, int delta_softplus, void* y,
+                                  int64_t batch, int64_t K, int64_t channels, int64_t L,
+                                  int64_t N, vmb_dtype in_dtype, vmb_dtype out_dtype,
+                                  vmb_layout layout, int64_t H, int64_t W, void* workspace,
+                                  size_t workspace_bytes, vmb_stream_t stream);
+
+/*
+ * VMeanba scan (Section 2.2, eq. 9): T averages the discretised scan inputs
+ * over the channels of each direction, the scan runs once per (b, k), and
+ * T^-1 broadcasts its output to every channel. With Delta as above and the
+ * sums over d = 0 .. channels-1 of direction k (c = k*channels + d):
+ *   Abar_mean[n,t] = mean_d exp(Delta_{d,t} * A[c,n])
+ *   s_mean[t]      = mean_d Delta_{d,t} * u[b,k,d,t]
+ *   r_mean[t]      = mean_d D[c] * u[b,k,d,t]
+ *   h_t[n]         = Abar_mean[n,t] * h_{t-1}[n] + B[b,k,n,t] * s_mean[t],  h_{-1} = 0
+ *   ytilde_t       = sum_n C[b,k,n,t] * h_t[n] + r_mean[t]
+ *   y[b,k,d,t]     = ytilde_t for every d              (SEQ)
+ *   y[b,d,h,w]     = cross-merge of ytilde over k      (2D, same for every d)
+ * Arguments, shapes, dtypes and workspace rules are those of
+ * vmb_selective_scan_fwd (workspace sized by vmb_scan_workspace_bytes(1, ...)).
+ * Channel sums are binary32 in a fixed order (deterministic).
+ */
+vmb_status vmb_mean_scan_fwd(const void* u, const void* delta, const float* A, const void* B,
+                             const void* C, const float* D, const float* dt_bias,
+                             int delta_softplus, void* y, int64_t batch, int64_t K,
+                             int64_t channels, int64_t L, int64_t N, vmb_dtype in_dtype,
+                             vmb_dtype out_dtype, vmb_layout layout, int64_t H, int64_t W,
+                             void* workspace, size_t workspace_bytes, vmb_stream_t stream);
+
+/*
+ * Bytes of device workspace the scan of the given shape needs
+ * (mean_variant = 0: vmb_selective_scan_fwd, 1: vmb_mean_scan_fwd).
+ * Returns 0 when none is needed and SIZE_MAX for an invalid shape.
+ */
+size_t vmb_scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
+                                int64_t L, int64_t N, vmb_layout layout);
+
+/* Static, NUL-terminated description of a status code. */
+const char* vmb_status_string(vmb_status s);
+
+/* VMB_ABI_VERSION of the loaded library. */
+int vmb_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VMB_H */

@@ -1,0 +1,138 @@
+// vmb_validate.cpp -- host-side argument checks of the libvmb entry points.
+// Pure C++: no HIP calls, so every error path can be exercised without a GPU.
+#include <stdint.h>
+
+#include <limits>
+
+#include "vmb_internal.h"
+
+namespace vmb {
+namespace {
+
+constexpr int64_t kMaxRow = (int64_t{1} << 31) - 1;   // elements per [.., L] row
+constexpr int64_t kMaxTotal = int64_t{1} << 40;       // elements per tensor
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t dsize(vmb_dtype t) { return t == VMB_BF16 ? 2 : 4; }
+
+bool valid_dtype(vmb_dtype t) { return t == VMB_F32 || t == VMB_BF16; }
+
+// overflow-checked product of positive sizes; returns -1 past kMaxTotal
+int64_t prod(std::initializer_list<int64_t> v) {
+    int64_t r = 1;
+    for (int64_t x : v) {
+        if (x <= 0) return -1;
+        if (r > kMaxTotal / x) return -1;
+        r *= x;
+    }
+    return r;
+}
+
+struct Range {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void* p, int64_t elems, size_t esz) {
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Range{lo, lo + static_cast<uintptr_t>(elems) * esz};
+}
+
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+bool supported_n(int64_t N) { return N == 1 || N == 2 || N == 4 || N == 8 || N == 16; }
+
+}  // namespace
+
+vmb_status validate_cross(const void* in, const void* out, int64_t batch, int64_t channels,
+                          int64_t H, int64_t W, vmb_dtype dt, bool unfold) {
+    if (!in || !out) return VMB_ERR_NULL;
+    if (!valid_dtype(dt)) return VMB_ERR_DTYPE;
+    if (batch < 1 || channels < 1 || H < 1 || W < 1) return VMB_ERR_SHAPE;
+    const int64_t L = prod({H, W});
+    if (L < 0 || L > kMaxRow) return VMB_ERR_SHAPE;
+    const int64_t n_map = prod({batch, channels, L});
+    const int64_t n_seq = prod({batch, 4, channels, L});
+    if (n_map < 0 || n_seq < 0) return VMB_ERR_SHAPE;
+    if (!aligned(in, 16) || !aligned(out, 16)) return VMB_ERR_ALIGN;
+    const size_t e = dsize(dt);
+    const Range rin = range_of(in, unfold ? n_map : n_seq, e);
+    const Range rout = range_of(out, unfold ? n_seq : n_map, e);
+    if (overlap(rin, rout)) return VMB_ERR_ALIAS;
+    return VMB_OK;
+}
+
+size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
+                            int64_t L, int64_t N, vmb_layout layout) {
+    if (batch < 1 || K < 1 || channels < 1 || L < 1 || N < 1) return SIZE_MAX;
+    const int64_t seq = prod({batch, K, channels, L});
+    if (seq < 0) return SIZE_MAX;
+    auto round_up = [](size_t v) { return (v + 255) & ~size_t{255}; };
+    if (!mean_variant) {
+        // 2-D layout: per-direction fp32 outputs, folded by the merge pass
+        return layout == VMB_LAYOUT_2D ? round_up(static_cast<size_t>(seq) * 4) : 0;
+    }
+    const int64_t nchunks = (L + kMeanChunk - 1) / kMeanChunk;
+    size_t bytes = 0;
+    bytes += round_up(static_cast<size_t>(batch * K * (N + 2) * L) * 4);       // reduced tile
+    bytes += round_up(static_cast<size_t>(batch * K * nchunks * N) * 2 * 4);   // chunk aggregates
+    bytes += round_up(static_cast<size_t>(batch * K * nchunks * N) * 4);       // chunk carries
+    if (layout == VMB_LAYOUT_2D) bytes += round_up(static_cast<size_t>(batch * K * L) * 4);
+    return bytes;
+}
+
+vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
+    if (!a.u || !a.delta || !a.A || !a.B || !a.C || !a.y) return VMB_ERR_NULL;
+    if (!valid_dtype(a.in_dt) || !valid_dtype(a.out_dt)) return VMB_ERR_DTYPE;
+    if (a.in_dt == VMB_F32 && a.out_dt == VMB_BF16) return VMB_ERR_DTYPE;
+    if (a.layout != VMB_LAYOUT_SEQ && a.layout != VMB_LAYOUT_2D) return VMB_ERR_SHAPE;
+    if (a.batch < 1 || a.K < 1 || a.channels < 1 || a.L < 1 || a.N < 1) return VMB_ERR_SHAPE;
+    if (a.L > kMaxRow) return VMB_ERR_SHAPE;
+    const int64_t seq = prod({a.batch, a.K, a.channels, a.L});
+    const int64_t bc = prod({a.batch, a.K, a.N, a.L});
+    const int64_t kc = prod({a.K, a.channels});
+    if (seq < 0 || bc < 0 || kc < 0 || kc > kMaxRow) return VMB_ERR_SHAPE;
+    // B and C are indexed n*L + t inside one (batch, direction) block
+    if (prod({a.N, a.L}) > kMaxRow) return VMB_ERR_SHAPE;
+    if (a.layout == VMB_LAYOUT_2D) {
+        if (a.K != 4 || a.H < 1 || a.W < 1 || prod({a.H, a.W}) != a.L) return VMB_ERR_SHAPE;
+    }
+    if (!supported_n(a.N)) return VMB_ERR_UNSUPPORTED;
+    // the chunk-local index math of the mean variant's passes is 32-bit
+    if (mean_variant && prod({a.batch, a.K, a.N + 2, a.L}) > kMaxRow) return VMB_ERR_UNSUPPORTED;
+    const void* streamed[] = {a.u, a.delta, a.B, a.C, a.y};
+    for (const void* p : streamed)
+        if (!aligned(p, 16)) return VMB_ERR_ALIGN;
+    if (!aligned(a.A, 4) || (a.D && !aligned(a.D, 4)) || (a.dt_bias && !aligned(a.dt_bias, 4)))
+        return VMB_ERR_ALIGN;
+    const size_t need = scan_workspace_bytes(mean_variant, a.batch, a.K, a.channels, a.L, a.N,
+                                             a.layout);
+    if (need == SIZE_MAX) return VMB_ERR_SHAPE;
+    if (need > 0) {
+        if (!a.ws || a.ws_bytes < need) return VMB_ERR_WORKSPACE;
+        if (!aligned(a.ws, 16)) return VMB_ERR_ALIGN;
+    }
+    // aliasing: the output must not overlap any input (or the workspace)
+    const size_t ein = dsize(a.in_dt), eout = dsize(a.out_dt);
+    const int64_t u_elems = a.layout == VMB_LAYOUT_2D ? seq / a.K : seq;
+    const int64_t y_elems = a.layout == VMB_LAYOUT_2D ? seq / a.K : seq;
+    const Range ry = range_of(a.y, y_elems, eout);
+    const Range inputs[] = {range_of(a.u, u_elems, ein),
+                            range_of(a.delta, seq, ein),
+                            range_of(a.B, bc, ein),
+                            range_of(a.C, bc, ein),
+                            range_of(a.A, kc * a.N, 4),
+                            a.D ? range_of(a.D, kc, 4) : Range{0, 0},
+                            a.dt_bias ? range_of(a.dt_bias, kc, 4) : Range{0, 0}};
+    for (const Range& r : inputs)
+        if (r.hi > r.lo && overlap(ry, r)) return VMB_ERR_ALIAS;
+    if (need > 0) {
+        const Range rw = range_of(a.ws, static_cast<int64_t>(need), 1);
+        if (overlap(ry, rw)) return VMB_ERR_ALIAS;
+        for (const Range& r : inputs)
+            if (r.hi > r.lo && overlap(rw, r)) return VMB_ERR_ALIAS;
+    }
+    return VMB_OK;
+}
+
+}  // namespace vmb

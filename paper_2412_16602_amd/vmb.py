@@ -1,0 +1,204 @@
+"""Python binding of libvmb (ctypes). Argument marshalling only.
+
+Each function takes torch tensors that already live on the GPU, checks that
+they are contiguous CUDA (HIP) tensors of the expected element type, and
+passes raw device pointers, sizes and the current HIP stream to the C entry
+point of the same name; every step of the computation runs in the HIP
+kernels. A non-OK status raises ``VmbError``. There is no CPU fallback: if
+the library is missing or was not built, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libvmb.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vmb.h")
+
+VMB_F32, VMB_BF16 = 0, 1
+VMB_LAYOUT_SEQ, VMB_LAYOUT_2D = 0, 1
+
+STATUS = {0: "VMB_OK", 1: "VMB_ERR_NULL", 2: "VMB_ERR_SHAPE", 3: "VMB_ERR_DTYPE",
+          4: "VMB_ERR_ALIGN", 5: "VMB_ERR_ALIAS", 6: "VMB_ERR_UNSUPPORTED",
+          7: "VMB_ERR_WORKSPACE", 8: "VMB_ERR_HIP"}
+
+
+class VmbError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({status_string(status)})")
+
+
+_lib = None
+
+
+def load_library():
+    """Load libvmb.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libvmb.so not found at {LIB_PATH}; run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    cross = [P, P, I64, I64, I64, I64, I, P]
+    for name in ("vmb_cross_scan", "vmb_cross_merge"):
+        fn = getattr(lib, name)
+        fn.argtypes = cross
+        fn.restype = I
+    scan = [P, P, P, P, P, P, P, I, P, I64, I64, I64, I64, I64, I, I, I, I64, I64, P,
+            ctypes.c_size_t, P]
+    for name in ("vmb_selective_scan_fwd", "vmb_mean_scan_fwd"):
+        fn = getattr(lib, name)
+        fn.argtypes = scan
+        fn.restype = I
+    lib.vmb_scan_workspace_bytes.argtypes = [I, I64, I64, I64, I64, I64, I]
+    lib.vmb_scan_workspace_bytes.restype = ctypes.c_size_t
+    lib.vmb_status_string.argtypes = [I]
+    lib.vmb_status_string.restype = ctypes.c_char_p
+    lib.vmb_abi_version.argtypes = []
+    lib.vmb_abi_version.restype = I
+    _lib = lib
+    return lib
+
+
+def declared_symbols() -> list[str]:
+    """Function names declared in include/vmb.h."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(vmb_[a-z_0-9]+)\s*\(", text)))
+
+
+def status_string(status: int) -> str:
+    try:
+        return load_library().vmb_status_string(int(status)).decode()
+    except Exception:  # the message is best-effort; the code is in the exception
+        return "?"
+
+
+def abi_version() -> int:
+    return int(load_library().vmb_abi_version())
+
+
+# ---------------------------------------------------------------- helpers
+
+_DT = {torch.float32: VMB_F32, torch.bfloat16: VMB_BF16}
+
+
+def _dev(t: Optional[torch.Tensor], name: str):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype(t: torch.Tensor, name: str) -> int:
+    if t.dtype not in _DT:
+        raise ValueError(f"{name}: unsupported dtype {t.dtype}")
+    return _DT[t.dtype]
+
+
+def _f32(t: Optional[torch.Tensor], name: str):
+    if t is not None and t.dtype != torch.float32:
+        raise ValueError(f"{name} must be float32")
+    return _dev(t, name)
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(int(stream.cuda_stream))
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise VmbError(status, where)
+
+
+# ---------------------------------------------------------------- entry points
+
+def vmb_cross_scan(x: torch.Tensor, xs: torch.Tensor, stream=None) -> torch.Tensor:
+    """x [batch, channels, H, W] -> xs [batch, 4, channels, H*W] (same dtype)."""
+    lib = load_library()
+    batch, channels, H, W = x.shape
+    dt = _dtype(x, "x")
+    if xs.dtype != x.dtype:
+        raise ValueError("xs must have the dtype of x")
+    if tuple(xs.shape) != (batch, 4, channels, H * W):
+        raise ValueError(f"xs shape {tuple(xs.shape)} != {(batch, 4, channels, H * W)}")
+    _check(lib.vmb_cross_scan(_dev(x, "x"), _dev(xs, "xs"), batch, channels, H, W, dt,
+                              _stream(stream)), "vmb_cross_scan")
+    return xs
+
+
+def vmb_cross_merge(ys: torch.Tensor, y: torch.Tensor, stream=None) -> torch.Tensor:
+    """ys [batch, 4, channels, H*W] -> y [batch, channels, H, W] (same dtype)."""
+    lib = load_library()
+    batch, channels, H, W = y.shape
+    dt = _dtype(ys, "ys")
+    if y.dtype != ys.dtype:
+        raise ValueError("y must have the dtype of ys")
+    if tuple(ys.shape) != (batch, 4, channels, H * W):
+        raise ValueError(f"ys shape {tuple(ys.shape)} != {(batch, 4, channels, H * W)}")
+    _check(lib.vmb_cross_merge(_dev(ys, "ys"), _dev(y, "y"), batch, channels, H, W, dt,
+                               _stream(stream)), "vmb_cross_merge")
+    return y
+
+
+def vmb_scan_workspace_bytes(mean_variant: bool, batch: int, K: int, channels: int, L: int,
+                             N: int, layout: int = VMB_LAYOUT_SEQ) -> int:
+    return int(load_library().vmb_scan_workspace_bytes(int(bool(mean_variant)), batch, K,
+                                                       channels, L, N, layout))
+
+
+def _scan(name, mean_variant, u, delta, A, B, C, D, dt_bias, delta_softplus, y, layout,
+          workspace, stream):
+    lib = load_library()
+    batch, K, channels, L = delta.shape
+    N = A.shape[1]
+    in_dt = _dtype(delta, "delta")
+    out_dt = _dtype(y, "y")
+    for t, nm in ((u, "u"), (B, "B"), (C, "C")):
+        if t.dtype != delta.dtype:
+            raise ValueError(f"{nm} must have the dtype of delta")
+    if layout == VMB_LAYOUT_2D:
+        if u.dim() != 4 or u.shape[0] != batch or u.shape[1] != channels:
+            raise ValueError("2-D layout: u must be x [batch, channels, H, W]")
+        H, W = int(u.shape[2]), int(u.shape[3])
+    else:
+        H, W = 1, L
+    if workspace is None:
+        need = vmb_scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=delta.device) if need else None
+    ws_ptr = _dev(workspace, "workspace")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    status = getattr(lib, name)(
+        _dev(u, "u"), _dev(delta, "delta"), _f32(A, "A"), _dev(B, "B"), _dev(C, "C"),
+        _f32(D, "D"), _f32(dt_bias, "dt_bias"), int(bool(delta_softplus)), _dev(y, "y"),
+        batch, K, channels, L, N, in_dt, out_dt, layout, H, W, ws_ptr, ws_bytes, _stream(stream))
+    _check(status, name)
+    return y
+
+
+def vmb_selective_scan_fwd(u, delta, A, B, C, D, dt_bias, delta_softplus, y,
+                           layout: int = VMB_LAYOUT_SEQ, workspace=None, stream=None):
+    """Full selective scan; shapes as in include/vmb.h. Returns y."""
+    return _scan("vmb_selective_scan_fwd", False, u, delta, A, B, C, D, dt_bias, delta_softplus,
+                 y, layout, workspace, stream)
+
+
+def vmb_mean_scan_fwd(u, delta, A, B, C, D, dt_bias, delta_softplus, y,
+                      layout: int = VMB_LAYOUT_SEQ, workspace=None, stream=None):
+    """VMeanba channel-mean scan; shapes as in include/vmb.h. Returns y."""
+    return _scan("vmb_mean_scan_fwd", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
+                 y, layout, workspace, stream)

@@ -1,0 +1,122 @@
+"""The C ABI on the CPU: the library loads, exports every function the
+header declares, and rejects bad arguments with the documented status before
+launching anything (the pointers below are never dereferenced)."""
+import ctypes
+
+import pytest
+
+from paper_2412_16602_amd import vmb
+
+OK, NULL, SHAPE, DTYPE, ALIGN, ALIAS, UNSUP, WS = 0, 1, 2, 3, 4, 5, 6, 7
+F32, BF16 = 0, 1
+SEQ, TWO_D = 0, 1
+
+
+@pytest.fixture(scope="module")
+def lib():
+    # The calls below pass fake device addresses that validation must reject
+    # before any launch. Never run them where a GPU could execute a kernel.
+    import torch
+    if torch.cuda.device_count() > 0:
+        pytest.skip("fake-pointer validation tests run on CPU-only hosts")
+    return vmb.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = vmb.declared_symbols()
+    assert set(names) >= {"vmb_cross_scan", "vmb_cross_merge", "vmb_selective_scan_fwd",
+                          "vmb_mean_scan_fwd", "vmb_scan_workspace_bytes", "vmb_status_string",
+                          "vmb_abi_version"}
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert vmb.abi_version() == 1
+    for s in range(9):
+        assert lib.vmb_status_string(s)
+    assert lib.vmb_status_string(OK) == b"ok"
+
+
+# fake, well-separated, 256-aligned "device" addresses
+BASE = 1 << 40
+STEP = 1 << 36
+
+
+def P(i, off=0):
+    return ctypes.c_void_p(BASE + i * STEP + off)
+
+
+def scan_call(lib, fn="vmb_selective_scan_fwd", **kw):
+    a = dict(u=P(0), delta=P(1), A=P(2), B=P(3), C=P(4), D=P(5), dt_bias=P(6), sp=1, y=P(7),
+             batch=1, K=4, channels=8, L=12, N=4, in_dt=F32, out_dt=F32, layout=SEQ, H=3, W=4,
+             ws=P(8), ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return getattr(lib, fn)(a["u"], a["delta"], a["A"], a["B"], a["C"], a["D"], a["dt_bias"],
+                            a["sp"], a["y"], a["batch"], a["K"], a["channels"], a["L"], a["N"],
+                            a["in_dt"], a["out_dt"], a["layout"], a["H"], a["W"], a["ws"],
+                            a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("fn", ["vmb_selective_scan_fwd", "vmb_mean_scan_fwd"])
+@pytest.mark.parametrize("kw,expect", [
+    (dict(u=None), NULL), (dict(delta=None), NULL), (dict(A=None), NULL), (dict(B=None), NULL),
+    (dict(C=None), NULL), (dict(y=None), NULL),
+    (dict(batch=0), SHAPE), (dict(K=0), SHAPE), (dict(channels=-1), SHAPE), (dict(L=0), SHAPE),
+    (dict(N=0), SHAPE), (dict(layout=7), SHAPE),
+    (dict(layout=TWO_D, K=3), SHAPE), (dict(layout=TWO_D, H=5, W=4), SHAPE),
+    (dict(N=3), UNSUP), (dict(N=32), UNSUP),
+    (dict(in_dt=2), DTYPE), (dict(out_dt=5), DTYPE), (dict(in_dt=F32, out_dt=BF16), DTYPE),
+    (dict(u=P(0, 4)), ALIGN), (dict(y=P(7, 8)), ALIGN), (dict(B=P(3, 2)), ALIGN),
+    (dict(A=P(2, 2)), ALIGN),
+    (dict(y=P(0, 16)), ALIAS), (dict(y=P(3)), ALIAS), (dict(y=P(2)), ALIAS),
+])
+def test_scan_rejects(lib, fn, kw, expect):
+    assert scan_call(lib, fn, **kw) == expect
+
+
+def test_workspace_rules(lib):
+    need_full_2d = lib.vmb_scan_workspace_bytes(0, 1, 4, 8, 12, 4, TWO_D)
+    need_mean = lib.vmb_scan_workspace_bytes(1, 1, 4, 8, 12, 4, SEQ)
+    assert lib.vmb_scan_workspace_bytes(0, 1, 4, 8, 12, 4, SEQ) == 0
+    assert need_full_2d >= 4 * 8 * 12 * 4 and need_mean > 0
+    assert scan_call(lib, layout=TWO_D, ws=None) == WS
+    assert scan_call(lib, layout=TWO_D, ws_bytes=need_full_2d - 1) == WS
+    assert scan_call(lib, "vmb_mean_scan_fwd", ws=None) == WS
+    assert scan_call(lib, "vmb_mean_scan_fwd", ws_bytes=need_mean - 1) == WS
+    assert scan_call(lib, "vmb_mean_scan_fwd", ws=P(8, 8)) == ALIGN
+    # workspace overlapping the output or an input
+    assert scan_call(lib, "vmb_mean_scan_fwd", ws=P(7)) == ALIAS
+    assert scan_call(lib, "vmb_mean_scan_fwd", ws=P(1)) == ALIAS
+    assert lib.vmb_scan_workspace_bytes(1, 0, 4, 8, 12, 4, SEQ) == ctypes.c_size_t(-1).value
+
+
+def test_shape_limits(lib):
+    assert scan_call(lib, L=1 << 31) == SHAPE
+    assert scan_call(lib, batch=1 << 20, channels=1 << 20) == SHAPE
+    assert scan_call(lib, N=16, L=(1 << 31) // 8) == SHAPE
+
+
+@pytest.mark.parametrize("fn,unfold", [("vmb_cross_scan", True), ("vmb_cross_merge", False)])
+def test_cross_rejects(lib, fn, unfold):
+    f = getattr(lib, fn)
+    assert f(None, P(1), 1, 2, 3, 4, F32, None) == NULL
+    assert f(P(0), None, 1, 2, 3, 4, F32, None) == NULL
+    assert f(P(0), P(1), 0, 2, 3, 4, F32, None) == SHAPE
+    assert f(P(0), P(1), 1, 2, 0, 4, F32, None) == SHAPE
+    assert f(P(0), P(1), 1, 2, 3, 4, 9, None) == DTYPE
+    assert f(P(0, 2), P(1), 1, 2, 3, 4, BF16, None) == ALIGN
+    assert f(P(0), P(1, 4), 1, 2, 3, 4, F32, None) == ALIGN
+    # overlap: map is 1*2*12 floats = 96 B, sequences 4x that
+    assert f(P(0), P(0, 64), 1, 2, 3, 4, F32, None) == ALIAS
+    if not unfold:
+        # merge input is the 4-direction tensor (384 B): an output 256 B in overlaps it
+        assert f(P(0), P(0, 256), 1, 2, 3, 4, F32, None) == ALIAS
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 2, 3, 4)
+    xs = torch.zeros(1, 4, 2, 12)
+    with pytest.raises(ValueError):
+        vmb.vmb_cross_scan(x, xs)
