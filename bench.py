@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""Benchmark of the SS2D selective-scan path on one MI355X.
+
+Workload: VMamba-T stage 1, batch 1, 56x56 feature map (L = 3136), K = 4
+directions, 192 channels, N = 16 states, fp32, seeded synthetic inputs
+(workloads.STAGE1).
+
+A step is one SS2D forward of the whole path, x [1, 192, 56, 56] -> y of the
+same shape: cross-scan fused into the scan's loads, the scan, and the
+cross-merge, via one vmb_selective_scan_fwd call in the 2-D layout (full
+variant). The same step with vmb_mean_scan_fwd (VMeanba) is timed next to it.
+Inputs are resident in HBM before timing starts; each step reads a different
+copy of the inputs (rotation over enough copies to exceed the 256 MB Infinity
+Cache), so every step streams from HBM.
+
+Prints one JSON line (rank 0). The `roofline` object covers the dominant
+kernel, the full scan, timed alone on the sequence layout with HIP events on
+its stream; `cpu_baseline` times the fp64 oracle on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = ("SS2D selective-scan µs/call + HBM GB/s (% peak), full vs mean, "
+          "VMamba-T 56×56")
+ROTATE_BYTES = 768 << 20  # > 2x the 256 MB MALL
+
+
+def seq_bytes(s: workloads.Shape, batch: int, esz_in=4, esz_out=4) -> int:
+    """Algorithmic bytes of one scan call, sequence layout: u, delta, B, C read
+    once, y written once (A, D, dt_bias included)."""
+    K, Dc, L, N = 4, s.channels, s.L, s.N
+    return (2 * batch * K * Dc * L + 2 * batch * K * N * L) * esz_in + batch * K * Dc * L * esz_out \
+        + (K * Dc * N + 2 * K * Dc) * 4
+
+
+def ss2d_bytes(s: workloads.Shape, batch: int, esz_in=4, esz_out=4) -> int:
+    """Algorithmic bytes of one SS2D forward, 2-D layout: x read once, delta,
+    B, C read once, merged y written once."""
+    K, Dc, L, N = 4, s.channels, s.L, s.N
+    return (batch * Dc * L + batch * K * Dc * L + 2 * batch * K * N * L) * esz_in \
+        + batch * Dc * L * esz_out + (K * Dc * N + 2 * K * Dc) * 4
+
+
+def gpu_bench(args):
+    import torch
+
+    from paper_2412_16602_amd import vmb
+
+    dev = torch.device("cuda:0")
+    shape = workloads.STAGE1
+    stream = torch.cuda.current_stream()
+
+    def upload(inp, layout):
+        g = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        u = g(inp.x if layout == "2d" else inp.u)
+        return dict(u=u, delta=g(inp.delta), A=g(inp.A), B=g(inp.B), C=g(inp.C), D=g(inp.D),
+                    dt_bias=g(inp.dt_bias))
+
+    inp2d = workloads.make_inputs(shape, "2d")
+    inpseq = workloads.make_inputs(shape, "seq")
+    step_bytes = ss2d_bytes(shape, shape.batch)
+    scan_bytes = seq_bytes(shape, shape.batch)
+    n_rot = max(2, -(-ROTATE_BYTES // step_bytes))
+
+    def make_sets(inp, layout, variant, n):
+        base = upload(inp, layout)
+        out_shape = tuple(inp.x.shape) if layout == "2d" else tuple(inp.delta.shape)
+        lay = vmb.VMB_LAYOUT_2D if layout == "2d" else vmb.VMB_LAYOUT_SEQ
+        need = vmb.vmb_scan_workspace_bytes(variant == "mean", shape.batch, 4, shape.channels,
+                                            shape.L, shape.N, lay)
+        sets = []
+        for i in range(n):
+            d = {k: (v.clone() if i else v) for k, v in base.items()}
+            d["y"] = torch.empty(out_shape, dtype=torch.float32, device=dev)
+            d["ws"] = torch.empty(max(need, 1), dtype=torch.uint8, device=dev) if need else None
+            sets.append(d)
+        return sets, lay
+
+    def runner(variant, sets, lay):
+        fn = vmb.vmb_selective_scan_fwd if variant == "full" else vmb.vmb_mean_scan_fwd
+
+        def call(i):
+            d = sets[i % len(sets)]
+            fn(d["u"], d["delta"], d["A"], d["B"], d["C"], d["D"], d["dt_bias"], True, d["y"],
+               layout=lay, workspace=d["ws"], stream=stream)
+        return call
+
+    def timed(call, steps, warmup):
+        for i in range(warmup):
+            call(i)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(steps):
+            call(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps  # us per call
+
+    res = {}
+    # --- the step: SS2D forward, 2-D layout, full and mean
+    for variant in ("full", "mean"):
+        sets, lay = make_sets(inp2d, "2d", variant, n_rot)
+        call = runner(variant, sets, lay)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        us = timed(call, args.steps, args.warmup)
+        wall = time.perf_counter() - t0
+        warm = timed(runner(variant, sets[:1], lay), args.steps, 2)
+        res[f"ss2d_{variant}"] = dict(us=us, warm_us=warm, wall_s=wall)
+        del sets
+    # --- dominant kernel alone: the scan, sequence layout (one kernel per call for full)
+    for variant in ("full", "mean"):
+        n = max(2, -(-ROTATE_BYTES // scan_bytes))
+        sets, lay = make_sets(inpseq, "seq", variant, n)
+        us = timed(runner(variant, sets, lay), args.steps, args.warmup)
+        res[f"seq_{variant}"] = dict(us=us)
+        del sets
+    torch.cuda.synchronize()
+    return res, step_bytes, scan_bytes, n_rot
+
+
+def cpu_baseline(budget_s: float):
+    """The fp64 oracle on the host: one SS2D forward (cross-scan, full scan,
+    merge) at the bench workload, repeated until about budget_s seconds."""
+    import oracle
+
+    threads = len(os.sched_getaffinity(0))
+    threads = min(threads, int(os.environ.get("OMP_NUM_THREADS", threads)))
+    inp = workloads.make_inputs(workloads.STAGE1, "2d")
+    H, W = inp.shape.H, inp.shape.W
+    reps, t_total = 0, 0.0
+    while True:
+        t0 = time.perf_counter()
+        xs = oracle.cross_scan(inp.x)
+        ys = oracle.full_scan(xs, inp.delta, inp.A, inp.B, inp.C, inp.D, inp.dt_bias, True,
+                              nthreads=threads)
+        oracle.cross_merge(ys, H, W, "f64")
+        t_total += time.perf_counter() - t0
+        reps += 1
+        if t_total >= budget_s or reps >= 1000:
+            break
+    return dict(value=t_total / reps * 1e6, unit="us/call", cores=threads, kind="oracle",
+                sample=f"{reps} x one SS2D forward (cross-scan, full scan, merge) at 1x56x56, "
+                       f"192 channels, N=16, fp64")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this SS2D scan library runs on a single "
+              "MI355X and has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    res, step_bytes, scan_bytes, n_rot = gpu_bench(args)
+    full, mean = res["ss2d_full"], res["ss2d_mean"]
+    sfull, smean = res["seq_full"], res["seq_mean"]
+    kern_us = sfull["us"]
+    achieved = scan_bytes / (kern_us * 1e-6) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(full["us"], 3),
+        "unit": "us/call",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(full["us"] / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": workloads.STAGE1.name, "batch": 1, "H": 56, "W": 56,
+                   "channels": 192, "K": 4, "N": 16, "layout": "2d", "variant": "full",
+                   "input_copies_rotated": n_rot},
+        "gbps": round(step_bytes / (full["us"] * 1e-6) / 1e9, 1),
+        "hbm_frac": round(step_bytes / (full["us"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+        "warm_us": round(full["warm_us"], 3),
+        "mean": {"us": round(mean["us"], 3), "warm_us": round(mean["warm_us"], 3),
+                 "gbps": round(step_bytes / (mean["us"] * 1e-6) / 1e9, 1),
+                 "speedup_vs_full": round(full["us"] / mean["us"], 3)},
+        "seq_scan": {"full_us": round(sfull["us"], 3), "mean_us": round(smean["us"], 3),
+                     "bytes": scan_bytes,
+                     "full_gbps": round(scan_bytes / (sfull["us"] * 1e-6) / 1e9, 1),
+                     "mean_gbps": round(scan_bytes / (smean["us"] * 1e-6) / 1e9, 1),
+                     "mean_speedup": round(sfull["us"] / smean["us"], 3)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None, "kernel": "full scan, sequence layout",
+                     "algorithmic_bytes": scan_bytes, "avg_us": round(kern_us, 3)},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

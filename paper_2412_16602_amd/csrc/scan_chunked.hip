@@ -1,0 +1,449 @@
+// scan_chunked.hip -- full selective scan, positions spread over lanes.
+//
+// Same recurrence as scan_full.hip (Appendix A: eq. 3, eq. 4 first line,
+// eq. 6), organised for shapes with few channels and long sequences, where
+// one lane per channel would leave most of the machine idle.
+//
+// Work decomposition. A workgroup owns G channels of one (batch, direction);
+// each channel gets Wv waves, each lane a run of T consecutive positions, so
+// one pass ("chunk") covers Wv*64*T positions and longer sequences loop over
+// chunks. For every state n (outer loop) a lane
+//   1. forms a_i = exp(Delta_i A_n) and b_i = Delta_i B_i u_i for its T
+//      positions (kept in registers) and composes them into its run's
+//      aggregate (prod a, state reached from zero),
+//   2. joins the runs: an inclusive DPP scan of the aggregates across the 64
+//      lanes, then, through LDS, across the Wv waves of the channel and with
+//      the state carried in from the previous chunk,
+//   3. re-walks its run from the state entering it, accumulating
+//      y_i += C_i h_i.
+// The aggregate's product is exp(A_n * sum_i Delta_i) (one exp per run, not
+// per position). The pair combine is (a1, b1) then (a2, b2) ->
+// (a1 a2, a2 b1 + b2), associative (Appendix A: the associative scan Mamba
+// runs in its kernel). Per (position, state): mul, exp2, mul, 3 fma.
+//
+// B and C rows are shared by every channel of a direction. The workgroup
+// copies each state's slice of them once, with coalesced loads, into a
+// triple-buffered LDS stage two states ahead of use; lanes then read their
+// runs from LDS (stride-13 words: conflict-free). One barrier per state
+// orders the stage and the cross-wave exchange.
+//
+// Workgroups are numbered so that the ones sharing a (batch, direction), and
+// therefore B and C, land on the same XCD and its L2.
+#include "vmb_internal.h"
+
+namespace vmb {
+namespace {
+
+constexpr int kWave = 64;
+
+// DPP controls (GFX9 encoding)
+constexpr int kWaveShr1 = 0x138;
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp(float old, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                                 __builtin_bit_cast(int, v), kCtrl,
+                                                                 kRowMask, 0xf, false));
+}
+
+// Inclusive scan of (P, H) over the 64 lanes of the wave, in lane order,
+// combine (P1, H1) then (P2, H2) -> (P1 P2, P2 H1 + H2). Each step reads the
+// partner lane's values through DPP inside the arithmetic (v_fmac / v_mul
+// with a DPP source); a lane whose partner does not exist is not written,
+// which is the identity. Wait states: a VALU result read through DPP needs
+// two independent instructions (or s_nop) in between.
+__device__ __forceinline__ void wave_scan(float& P, float& Hs) {
+    asm volatile(
+        "s_nop 1\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+        "s_nop 1\n"
+        : "+v"(Hs), "+v"(P));
+}
+
+// T consecutive elements starting at p (element-aligned). full: all T are
+// in range; otherwise only the first cnt are read, the rest become 0.
+template <int T>
+__device__ __forceinline__ void load_run(const float* p, float (&v)[T], bool full, int cnt) {
+    if (full) {
+#pragma unroll
+        for (int i = 0; i + 4 <= T; i += 4) {
+            float4 q;
+            __builtin_memcpy(&q, p + i, 16);
+            v[i] = q.x;
+            v[i + 1] = q.y;
+            v[i + 2] = q.z;
+            v[i + 3] = q.w;
+        }
+#pragma unroll
+        for (int i = T & ~3; i < T; ++i) v[i] = p[i];
+    } else {
+#pragma unroll
+        for (int i = 0; i < T; ++i) v[i] = i < cnt ? p[i] : 0.0f;
+    }
+}
+
+template <int T>
+__device__ __forceinline__ void load_run(const bf16_t* p, float (&v)[T], bool full, int cnt) {
+    if (full) {
+#pragma unroll
+        for (int i = 0; i + 2 <= T; i += 2) {
+            uint32_t q;
+            __builtin_memcpy(&q, p + i, 4);
+            v[i] = __uint_as_float(q << 16);
+            v[i + 1] = __uint_as_float(q & 0xffff0000u);
+        }
+        if (T & 1) v[T - 1] = to_f32(p[T - 1]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < T; ++i) v[i] = i < cnt ? to_f32(p[i]) : 0.0f;
+    }
+}
+
+template <int T, typename Tout>
+__device__ __forceinline__ void store_run(Tout* p, const float (&v)[T], bool full, int cnt) {
+    if constexpr (sizeof(Tout) == 4) {
+        if (full) {
+#pragma unroll
+            for (int i = 0; i + 4 <= T; i += 4) {
+                const float4 q = make_float4(v[i], v[i + 1], v[i + 2], v[i + 3]);
+                __builtin_memcpy(p + i, &q, 16);
+            }
+#pragma unroll
+            for (int i = T & ~3; i < T; ++i) p[i] = v[i];
+            return;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < T; ++i)
+        if (full || i < cnt) p[i] = from_f32<Tout>(v[i]);
+}
+
+// u values of a run in the 2-D layout: position t of direction k reads pixel
+// pixel_of(k, t); rows are walked incrementally for the column-major maps.
+template <int T, typename Tin>
+__device__ __forceinline__ void load_run_2d(const Tin* plane, int k, int t0, int H, int W, int L,
+                                            float (&v)[T], int cnt) {
+    const int tt = (k >= 2) ? (L - 1 - t0) : t0;
+    if ((k & 1) == 0) {
+        const int step = (k >= 2) ? -1 : 1;
+#pragma unroll
+        for (int i = 0; i < T; ++i) v[i] = i < cnt ? to_f32(plane[tt + step * i]) : 0.0f;
+        return;
+    }
+    int w = tt / H;
+    int h = tt - w * H;
+    const bool rev = k >= 2;
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+        v[i] = i < cnt ? to_f32(plane[h * W + w]) : 0.0f;
+        if (!rev) {
+            if (++h == H) { h = 0; ++w; }
+        } else {
+            if (--h < 0) { h = H - 1; --w; }
+        }
+    }
+}
+
+// Phase 1 of one state for one lane: a_i, b_i of its run (registers), the
+// run aggregate, the inclusive scan over the wave, this wave's aggregate
+// published to xg[wv] by the last lane, and the lane's exclusive prefix
+// (Pex, Hex) kept for phase 2.
+template <int T, typename Tin>
+__device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], const float (&du)[T],
+                                             float s2, const Tin* bsrc, float (&a)[T],
+                                             float (&bu)[T], float& Pex, float& Hex,
+                                             float (*xg)[2], int lane, int wv) {
+    float agg = 0.0f;
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+        a[i] = fast_exp2(dl2[i] * an);
+        bu[i] = du[i] * to_f32(bsrc[i]);
+        agg = __builtin_fmaf(a[i], agg, bu[i]);
+    }
+    float P = fast_exp2(s2 * an);
+    float Hs = agg;
+    wave_scan(P, Hs);
+    if (lane == kWave - 1) {
+        xg[wv][0] = P;
+        xg[wv][1] = Hs;
+    }
+    // exclusive prefix of this lane: the inclusive one of lane - 1
+    Pex = dpp<kWaveShr1, 0xf>(1.0f, P);
+    Hex = dpp<kWaveShr1, 0xf>(0.0f, Hs);
+}
+
+// Phase 2 (after the workgroup barrier): state entering this wave from the
+// channel's earlier waves and the previous chunk, then the re-walk of the run
+// from the state entering this lane, accumulating y_i += C_i h_i. All waves
+// of a channel compose the same aggregates in the same order, so the state
+// carried to the next chunk is identical in each of them.
+template <int T, int kMaxWv, typename Tin>
+__device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pex,
+                                             float Hex, const Tin* csrc, float (&yv)[T],
+                                             const float (*xg)[2], float& hc, int lane, int g,
+                                             int w, int Wv) {
+    float xp[kMaxWv], xh[kMaxWv];
+#pragma unroll
+    for (int j = 0; j < kMaxWv; ++j) {
+        if (j < Wv) {
+            xp[j] = xg[g * Wv + j][0];
+            xh[j] = xg[g * Wv + j][1];
+        }
+    }
+    float cin = hc;
+    float cnext = cin;
+#pragma unroll
+    for (int j = 0; j < kMaxWv; ++j) {
+        if (j < Wv) {
+            cnext = __builtin_fmaf(xp[j], cnext, xh[j]);
+            if (j + 1 == w) cin = cnext;
+        }
+    }
+    if (w == 0) cin = hc;
+    if (lane == 0) hc = cnext;
+    float h = __builtin_fmaf(Pex, cin, Hex);
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+        h = __builtin_fmaf(a[i], h, bu[i]);
+        yv[i] = __builtin_fmaf(to_f32(csrc[i]), h, yv[i]);
+    }
+}
+
+// Slice of the B or C row of one state copied into LDS: positions
+// [cs, cs + len) of the row, len <= kStageMax. The copy goes straight from
+// global memory to LDS (gfx950 global_load_lds: each lane of a wave moves 16
+// or 4 bytes to LDS at base + lane * size), no registers involved. Rows whose
+// length is a multiple of 4 move 16-byte pieces, others single words. The
+// issuing wave must wait for vmcnt before the barrier that publishes them.
+constexpr int kStageMax = 4 * kWave * 13;
+constexpr int kStageThreads = 768;
+
+template <typename Tin>
+__device__ __forceinline__ void stage_row(const Tin* row, Tin* dst, int cs, int len, bool vec4,
+                                          int wv, int lane) {
+    // Only waves 0..3 issue copies (one per SIMD: a wave blocked on a full
+    // copy queue leaves its SIMD to the two other waves there).
+    constexpr int kIssuers = 4;
+    if (wv >= kIssuers) return;
+    constexpr int kEl = static_cast<int>(sizeof(Tin));
+    if (vec4) {
+        constexpr int kPer = 16 / kEl;          // elements per lane-piece
+        constexpr int kSpan = kWave * kPer;     // elements per wave-instruction
+        for (int base = wv * kSpan; base < len; base += kIssuers * kSpan) {
+            const int j = base + lane * kPer;
+            if (j < len)
+                __builtin_amdgcn_global_load_lds(row + cs + j, dst + base, 16, 0, 0);
+        }
+    } else {
+        constexpr int kPer = 4 / kEl;
+        constexpr int kSpan = kWave * kPer;
+        for (int base = wv * kSpan; base < len; base += kIssuers * kSpan) {
+            const int j = base + lane * kPer;
+            if (j < len)
+                __builtin_amdgcn_global_load_lds(row + cs + j, dst + base, 4, 0, 0);
+        }
+    }
+}
+
+// Row n0 + s of B or C for pair step p (chunk p / pairs, state
+// 2 * (p % pairs) + s), positions of that chunk, into dst.
+template <int kPairs, typename Tin>
+__device__ __forceinline__ void stage_one(const Tin* base, int p, int s, Tin* dst, int L, int chunk,
+                                          bool vec4, int wv, int lane) {
+    const int ci = p / kPairs, n0 = 2 * (p - ci * kPairs);
+    const int cs = ci * chunk;
+    const int len = L - cs < chunk ? L - cs : chunk;
+    stage_row(base + static_cast<size_t>(n0 + s) * L, dst, cs, len, vec4, wv, lane);
+}
+
+// Wait until this wave's outstanding vector-memory operations (including the
+// LDS copies above) are done: vmcnt(0), other counters untouched.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
+template <int N, int T, typename Tin, typename Tout, bool kTwoD>
+__global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
+    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
+    const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
+    const float* __restrict__ dt_bias, Tout* __restrict__ y, int K, int Dc, int L, int H, int W,
+    int softplus, int G, int Wv, int n_groups, int n_wg) {
+    static_assert(N % 2 == 0, "states are processed in pairs");
+    constexpr int kMaxWv = 4;
+    constexpr int kPairs = N / 2;
+    // per (parity, state of the pair, wave): aggregates exchanged across waves
+    __shared__ float xagg[2][2][16][2];
+    __shared__ float hcar[16][N];
+    // B and C slices of a pair of states, double-buffered (distinct arrays so
+    // that copies into one buffer never order reads of the other)
+    __shared__ Tin bst0[2][kStageMax], bst1[2][kStageMax];
+    __shared__ Tin cst0[2][kStageMax], cst1[2][kStageMax];
+
+    // XCD-aware numbering: hardware places workgroup i on XCD i % 8
+    const int bid = blockIdx.x;
+    const int per = n_wg / 8, rem = n_wg % 8;
+    const int xcd = bid % 8, slot = bid / 8;
+    const int logical = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+    const int dg = logical % n_groups;
+    const int bk = logical / n_groups;  // b * K + k
+    const int k = bk % K;
+    const int b = bk / K;
+
+    const int tid = threadIdx.x;
+    const int lane = tid % kWave;
+    const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int g = wv / Wv, w = wv - g * Wv;
+    const int d_raw = dg * G + g;
+    const bool d_ok = d_raw < Dc;
+    const int d = d_ok ? d_raw : Dc - 1;
+    const int c = k * Dc + d;
+    const size_t row = (static_cast<size_t>(bk) * Dc + d) * static_cast<size_t>(L);
+    const Tin* drow = delta + row;
+    const Tin* urow = kTwoD ? u + (static_cast<size_t>(b) * Dc + d) * L : u + row;
+    const Tin* Bb = Bm + static_cast<size_t>(bk) * N * L;
+    const Tin* Cb = Cm + static_cast<size_t>(bk) * N * L;
+    Tout* yrow = y + row;
+    const float bias = dt_bias ? dt_bias[c] : 0.0f;
+    const float dskip = D ? D[c] : 0.0f;
+    const bool sp = softplus != 0;
+    const float* Arow = A + static_cast<size_t>(c) * N;
+
+    const int chunk = Wv * kWave * T;
+    const int nchunks = (L + chunk - 1) / chunk;
+    const int npairs = nchunks * kPairs;  // step = (chunk, pair of states)
+    const bool vec4 = (L % (16 / static_cast<int>(sizeof(Tin)))) == 0;
+    const int run = (w * kWave + lane) * T;  // this lane's first position inside a chunk
+
+    auto stage = [&](const Tin* base, int p, int st, Tin* dst) {
+        stage_one<kPairs>(base, p, st, dst, L, chunk, vec4, wv, lane);
+    };
+
+    for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
+    stage(Bb, 0, 0, bst0[0]);
+    stage(Bb, 0, 1, bst0[1]);
+    stage(Cb, 0, 0, cst0[0]);
+    stage(Cb, 0, 1, cst0[1]);
+    if (npairs > 1) {
+        stage(Bb, 1, 0, bst1[0]);
+        stage(Bb, 1, 1, bst1[1]);
+    }
+    wait_vmem();
+    __syncthreads();
+
+    float dl2[T], du[T], yv[T];
+    float s2 = 0.0f;
+    int t0 = 0, cnt = 0;
+    bool full = false;
+
+    // One pair step. Stage schedule (one barrier per step): between this
+    // step's barrier and the next, the copies for C of pair p + 1 and B of
+    // pair p + 2 are issued, spread over phase 2 of this step and phase 1 of
+    // the next, into the buffers whose previous contents were last read
+    // before this step's barrier; they complete before the next barrier.
+    // bprev is the B buffer of the previous step (target of B of pair p + 1,
+    // whose last two rows are issued during this step's phase 1).
+    auto pair_step = [&](int p, Tin (*bcur)[kStageMax], Tin (*bprev)[kStageMax],
+                         Tin (*ccur)[kStageMax], Tin (*cnxt)[kStageMax]) {
+        const int ci = p / kPairs, n0 = 2 * (p - ci * kPairs);
+        if (n0 == 0) {
+            // new chunk: this lane's run of delta and u
+            t0 = ci * chunk + run;
+            cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
+            full = cnt == T;
+            const int tl = cnt > 0 ? t0 : 0;  // keep addresses in range for empty runs
+            float dv[T], uv[T];
+            load_run<T>(drow + tl, dv, full, cnt);
+            if constexpr (kTwoD)
+                load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
+            else
+                load_run<T>(urow + tl, uv, full, cnt);
+            s2 = 0.0f;
+#pragma unroll
+            for (int i = 0; i < T; ++i) {
+                // positions past the end act as the identity: a = 1, b = 0
+                const float dl = i < cnt ? timescale(dv[i] + bias, sp) : 0.0f;
+                dl2[i] = dl * kLog2e;
+                du[i] = dl * uv[i];
+                yv[i] = dskip * uv[i];
+                s2 += dl2[i];
+            }
+        }
+        float a0[T], bu0[T], a1[T], bu1[T];
+        float Pex0, Hex0, Pex1, Hex1;
+        state_phase1<T>(Arow[n0], dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0,
+                        xagg[p & 1][0], lane, wv);
+        // second half of the previous step's window: C of pair p (already
+        // issued) and the rest of B of pair p + 1
+        if (p >= 1 && p + 1 < npairs) stage(Bb, p + 1, 1, bprev[1]);
+        state_phase1<T>(Arow[n0 + 1], dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1,
+                        xagg[p & 1][1], lane, wv);
+        wait_vmem();
+        __syncthreads();
+        if (p + 1 < npairs) stage(Cb, p + 1, 0, cnxt[0]);
+        state_phase2<T, kMaxWv>(a0, bu0, Pex0, Hex0, &ccur[0][run], yv, xagg[p & 1][0],
+                                hcar[wv][n0], lane, g, w, Wv);
+        if (p + 1 < npairs) stage(Cb, p + 1, 1, cnxt[1]);
+        if (p + 2 < npairs) stage(Bb, p + 2, 0, bcur[0]);
+        state_phase2<T, kMaxWv>(a1, bu1, Pex1, Hex1, &ccur[1][run], yv, xagg[p & 1][1],
+                                hcar[wv][n0 + 1], lane, g, w, Wv);
+        if (n0 + 2 == N && d_ok && cnt > 0) store_run<T>(yrow + t0, yv, full, cnt);
+    };
+
+    for (int p = 0; p < npairs; p += 2) {
+        pair_step(p, bst0, bst1, cst0, cst1);
+        if (p + 1 < npairs) pair_step(p + 1, bst1, bst0, cst1, cst0);
+    }
+}
+
+}  // namespace
+
+// Chunked full scan: picks the run length and waves per channel from L.
+namespace {
+template <int N, typename Tin, typename Tout, bool kTwoD>
+vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y) {
+    const int L = int(a.L);
+    // waves per channel and run length: cover L with few idle lanes
+    // runs of 13 positions; waves per channel from L
+    constexpr int T = 13;
+    const int Wv = L > 2 * kWave * T ? 4 : (L > kWave * T ? 2 : 1);
+    const int G = Wv == 4 ? 3 : (Wv == 2 ? 6 : 12);  // channels per workgroup: 12 waves
+    const int n_groups = int((a.channels + G - 1) / G);
+    const long long n_wg = static_cast<long long>(n_groups) * a.K * a.batch;
+    if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
+    const dim3 grid(static_cast<unsigned>(n_wg)), block(kWave * G * Wv);
+    hipLaunchKernelGGL((k_full_scan_chunked<N, T, Tin, Tout, kTwoD>), grid, block, 0, a.stream,
+                       static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
+                       static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,
+                       y, int(a.K), int(a.channels), L, int(a.H), int(a.W), a.softplus, G, Wv,
+                       n_groups, int(n_wg));
+    return check_launch();
+}
+}  // namespace
+
+vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq) {
+    if (a.N != 16) return VMB_ERR_UNSUPPORTED;
+    const bool two_d = a.layout == VMB_LAYOUT_2D;
+    if (a.in_dt == VMB_F32)
+        return two_d ? launch_chunked_impl<16, float, float, true>(a, static_cast<float*>(y_seq))
+                     : launch_chunked_impl<16, float, float, false>(a, static_cast<float*>(y_seq));
+    if (two_d) return launch_chunked_impl<16, bf16_t, float, true>(a, static_cast<float*>(y_seq));
+    if (a.out_dt == VMB_BF16)
+        return launch_chunked_impl<16, bf16_t, bf16_t, false>(a, static_cast<bf16_t*>(y_seq));
+    return launch_chunked_impl<16, bf16_t, float, false>(a, static_cast<float*>(y_seq));
+}
+
+}  // namespace vmb

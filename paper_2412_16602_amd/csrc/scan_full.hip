@@ -99,7 +99,16 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 
 }  // namespace
 
+bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L >= 512; }
+
 vmb_status launch_full_scan(const ScanArgs& a) {
+    if (use_chunked_full(a)) {
+        if (a.layout == VMB_LAYOUT_SEQ) return launch_full_chunked(a, a.y);
+        vmb_status st = launch_full_chunked(a, a.ws);
+        if (st != VMB_OK) return st;
+        return launch_cross_merge(a.ws, a.y, a.batch, a.channels, a.H, a.W, VMB_F32, a.out_dt,
+                                  a.stream);
+    }
     if (a.batch > 65535 || a.K > 65535) return VMB_ERR_UNSUPPORTED;
     switch (a.N) {
         case 1: return dispatch_dtype<1>(a);

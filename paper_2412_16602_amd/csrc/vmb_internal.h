@@ -51,6 +51,11 @@ vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t ch
                               int64_t H, int64_t W, vmb_dtype in_dt, vmb_dtype out_dt,
                               hipStream_t s);
 vmb_status launch_full_scan(const ScanArgs& a);
+// Positions-over-lanes full scan (N == 16); writes sequence-layout output to
+// y_seq (a.y for the sequence layout, the fp32 workspace for the 2-D one).
+vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq);
+// Whether the positions-over-lanes kernel is the better fit for this shape.
+bool use_chunked_full(const ScanArgs& a);
 vmb_status launch_mean_scan(const ScanArgs& a);
 
 inline vmb_status check_launch() {

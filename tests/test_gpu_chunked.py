@@ -1,0 +1,66 @@
+"""Full scan on long sequences (the positions-over-lanes kernel): chunk and
+run boundaries, channel-group tails, dtypes and the 2-D layout."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from gpu_util import BF16_TOL, FP32_TOL, assert_close, log, oracle_seq, run_scan, to_f64
+from test_gpu_scan import merged_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def shape(b, H, W, c, dtype="f32", seed=0):
+    return workloads.custom_shape(b, H, W, c, 16, dtype, seed, True)
+
+
+# L chosen around the run / wave / chunk boundaries (runs of 13 or 16 positions,
+# 64 lanes per wave, 1, 2 or 4 waves per channel)
+LENGTHS = [512, 831, 832, 833, 1663, 1664, 1665, 3136, 3327, 3328, 3329, 4096, 4097, 8193]
+
+
+@pytest.mark.parametrize("L", LENGTHS)
+def test_lengths(L):
+    log(f"chunked full L={L}")
+    inp = workloads.make_inputs(shape(1, 1, L, 5, seed=L), "seq", d_value=0.0)
+    got = to_f64(run_scan(inp, "full", "seq"))
+    ref = oracle_seq(inp, "full", "seq")
+    assert_close(got, ref, **FP32_TOL, what=f"chunked L={L}")
+
+
+@pytest.mark.parametrize("channels", [1, 2, 3, 4, 7, 13])
+def test_channel_group_tails(channels):
+    log(f"chunked full channels={channels}")
+    inp = workloads.make_inputs(shape(2, 40, 50, channels, seed=100 + channels), "seq")
+    got = to_f64(run_scan(inp, "full", "seq"))
+    ref = oracle_seq(inp, "full", "seq")
+    assert_close(got, ref, **FP32_TOL, what=f"chunked channels={channels}")
+
+
+@pytest.mark.parametrize("out", ["bf16", "f32"])
+def test_bf16(out):
+    log(f"chunked full bf16 -> {out}")
+    inp = workloads.make_inputs(shape(1, 33, 61, 6, "bf16", seed=200), "seq")
+    y = run_scan(inp, "full", "seq", out_dtype=torch.bfloat16 if out == "bf16" else torch.float32)
+    ref = oracle_seq(inp, "full", "seq")
+    assert_close(to_f64(y), ref, **(BF16_TOL if out == "bf16" else FP32_TOL), what=f"bf16->{out}")
+
+
+@pytest.mark.parametrize("H,W", [(56, 56), (29, 31), (1, 700), (700, 1), (64, 130)])
+def test_2d_layout(H, W):
+    log(f"chunked full 2d {H}x{W}")
+    inp = workloads.make_inputs(shape(1, H, W, 4, seed=H * 1000 + W), "2d")
+    got = to_f64(run_scan(inp, "full", "2d"))
+    ref, scale = merged_oracle(inp, "full")
+    assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
+                 what=f"2d {H}x{W}")
+
+
+def test_softplus_off_and_no_bias():
+    log("chunked full softplus off")
+    inp = workloads.make_inputs(shape(1, 20, 60, 3, seed=300), "seq")
+    delta = (np.abs(inp.delta) * 0.05 + 1e-3).astype(np.float32)
+    got = to_f64(run_scan(inp, "full", "seq", softplus=False, use_bias=False, delta=delta))
+    ref = oracle_seq(inp, "full", "seq", softplus=False, use_bias=False, delta=delta)
+    assert_close(got, ref, **FP32_TOL, what="softplus off")
