@@ -47,13 +47,14 @@ __device__ __forceinline__ float dpp(float old, float v) {
 }
 
 // Inclusive scan of (P, H) over the 64 lanes of the wave, in lane order,
+// (plain asm: no side effects, so the scheduler may interleave other work)
 // combine (P1, H1) then (P2, H2) -> (P1 P2, P2 H1 + H2). Each step reads the
 // partner lane's values through DPP inside the arithmetic (v_fmac / v_mul
 // with a DPP source); a lane whose partner does not exist is not written,
 // which is the identity. Wait states: a VALU result read through DPP needs
 // two independent instructions (or s_nop) in between.
 __device__ __forceinline__ void wave_scan(float& P, float& Hs) {
-    asm volatile(
+    asm(
         "s_nop 1\n"
         "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
         "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
@@ -232,20 +233,18 @@ __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&
 // length is a multiple of 4 move 16-byte pieces, others single words. The
 // issuing wave must wait for vmcnt before the barrier that publishes them.
 constexpr int kStageMax = 4 * kWave * 13;
-constexpr int kStageThreads = 768;
+constexpr int kComputeWaves = 12;  // G channels x Wv waves
+constexpr int kCopyWaves = 4;      // one per SIMD, copies only
+constexpr int kStageThreads = (kComputeWaves + kCopyWaves) * kWave;
 
 template <typename Tin>
 __device__ __forceinline__ void stage_row(const Tin* row, Tin* dst, int cs, int len, bool vec4,
-                                          int wv, int lane) {
-    // Only waves 0..3 issue copies (one per SIMD: a wave blocked on a full
-    // copy queue leaves its SIMD to the two other waves there).
-    constexpr int kIssuers = 4;
-    if (wv >= kIssuers) return;
+                                          int issuer, int lane) {
     constexpr int kEl = static_cast<int>(sizeof(Tin));
     if (vec4) {
         constexpr int kPer = 16 / kEl;          // elements per lane-piece
         constexpr int kSpan = kWave * kPer;     // elements per wave-instruction
-        for (int base = wv * kSpan; base < len; base += kIssuers * kSpan) {
+        for (int base = issuer * kSpan; base < len; base += kCopyWaves * kSpan) {
             const int j = base + lane * kPer;
             if (j < len)
                 __builtin_amdgcn_global_load_lds(row + cs + j, dst + base, 16, 0, 0);
@@ -253,7 +252,7 @@ __device__ __forceinline__ void stage_row(const Tin* row, Tin* dst, int cs, int 
     } else {
         constexpr int kPer = 4 / kEl;
         constexpr int kSpan = kWave * kPer;
-        for (int base = wv * kSpan; base < len; base += kIssuers * kSpan) {
+        for (int base = issuer * kSpan; base < len; base += kCopyWaves * kSpan) {
             const int j = base + lane * kPer;
             if (j < len)
                 __builtin_amdgcn_global_load_lds(row + cs + j, dst + base, 4, 0, 0);
@@ -265,11 +264,11 @@ __device__ __forceinline__ void stage_row(const Tin* row, Tin* dst, int cs, int 
 // 2 * (p % pairs) + s), positions of that chunk, into dst.
 template <int kPairs, typename Tin>
 __device__ __forceinline__ void stage_one(const Tin* base, int p, int s, Tin* dst, int L, int chunk,
-                                          bool vec4, int wv, int lane) {
+                                          bool vec4, int issuer, int lane) {
     const int ci = p / kPairs, n0 = 2 * (p - ci * kPairs);
     const int cs = ci * chunk;
     const int len = L - cs < chunk ? L - cs : chunk;
-    stage_row(base + static_cast<size_t>(n0 + s) * L, dst, cs, len, vec4, wv, lane);
+    stage_row(base + static_cast<size_t>(n0 + s) * L, dst, cs, len, vec4, issuer, lane);
 }
 
 // Wait until this wave's outstanding vector-memory operations (including the
@@ -306,6 +305,40 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int chunk = Wv * kWave * T;
+    const int nchunks = (L + chunk - 1) / chunk;
+    const int npairs = nchunks * kPairs;  // step = (chunk, pair of states)
+    const bool vec4 = (L % (16 / static_cast<int>(sizeof(Tin)))) == 0;
+    const Tin* Bb = Bm + static_cast<size_t>(bk) * N * L;
+    const Tin* Cb = Cm + static_cast<size_t>(bk) * N * L;
+
+    if (wv >= kComputeWaves) {
+        // Copy waves. Before barrier p they issue C of pair p and B of pair
+        // p + 1, into buffers last read before barrier p - 1, then wait for
+        // their completion; barrier p publishes them.
+        const int issuer = wv - kComputeWaves;
+        auto stage = [&](const Tin* base, int p, int st, Tin* dst) {
+            stage_one<kPairs>(base, p, st, dst, L, chunk, vec4, issuer, lane);
+        };
+        stage(Bb, 0, 0, bst0[0]);
+        stage(Bb, 0, 1, bst0[1]);
+        wait_vmem();
+        __syncthreads();
+        for (int p = 0; p < npairs; ++p) {
+            Tin (*cdst)[kStageMax] = (p & 1) ? cst1 : cst0;
+            Tin (*bdst)[kStageMax] = (p & 1) ? bst0 : bst1;
+            stage(Cb, p, 0, cdst[0]);
+            stage(Cb, p, 1, cdst[1]);
+            if (p + 1 < npairs) {
+                stage(Bb, p + 1, 0, bdst[0]);
+                stage(Bb, p + 1, 1, bdst[1]);
+            }
+            wait_vmem();
+            __syncthreads();
+        }
+        return;
+    }
+
     const int g = wv / Wv, w = wv - g * Wv;
     const int d_raw = dg * G + g;
     const bool d_ok = d_raw < Dc;
@@ -314,34 +347,14 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const size_t row = (static_cast<size_t>(bk) * Dc + d) * static_cast<size_t>(L);
     const Tin* drow = delta + row;
     const Tin* urow = kTwoD ? u + (static_cast<size_t>(b) * Dc + d) * L : u + row;
-    const Tin* Bb = Bm + static_cast<size_t>(bk) * N * L;
-    const Tin* Cb = Cm + static_cast<size_t>(bk) * N * L;
     Tout* yrow = y + row;
     const float bias = dt_bias ? dt_bias[c] : 0.0f;
     const float dskip = D ? D[c] : 0.0f;
     const bool sp = softplus != 0;
     const float* Arow = A + static_cast<size_t>(c) * N;
-
-    const int chunk = Wv * kWave * T;
-    const int nchunks = (L + chunk - 1) / chunk;
-    const int npairs = nchunks * kPairs;  // step = (chunk, pair of states)
-    const bool vec4 = (L % (16 / static_cast<int>(sizeof(Tin)))) == 0;
     const int run = (w * kWave + lane) * T;  // this lane's first position inside a chunk
 
-    auto stage = [&](const Tin* base, int p, int st, Tin* dst) {
-        stage_one<kPairs>(base, p, st, dst, L, chunk, vec4, wv, lane);
-    };
-
     for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
-    stage(Bb, 0, 0, bst0[0]);
-    stage(Bb, 0, 1, bst0[1]);
-    stage(Cb, 0, 0, cst0[0]);
-    stage(Cb, 0, 1, cst0[1]);
-    if (npairs > 1) {
-        stage(Bb, 1, 0, bst1[0]);
-        stage(Bb, 1, 1, bst1[1]);
-    }
-    wait_vmem();
     __syncthreads();
 
     float dl2[T], du[T], yv[T];
@@ -349,15 +362,10 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     int t0 = 0, cnt = 0;
     bool full = false;
 
-    // One pair step. Stage schedule (one barrier per step): between this
-    // step's barrier and the next, the copies for C of pair p + 1 and B of
-    // pair p + 2 are issued, spread over phase 2 of this step and phase 1 of
-    // the next, into the buffers whose previous contents were last read
-    // before this step's barrier; they complete before the next barrier.
-    // bprev is the B buffer of the previous step (target of B of pair p + 1,
-    // whose last two rows are issued during this step's phase 1).
-    auto pair_step = [&](int p, Tin (*bcur)[kStageMax], Tin (*bprev)[kStageMax],
-                         Tin (*ccur)[kStageMax], Tin (*cnxt)[kStageMax]) {
+    // One pair step: phase 1 reads B of the pair (published by the previous
+    // barrier), the barrier publishes this step's wave aggregates and C of
+    // the pair, phase 2 reads them.
+    auto pair_step = [&](int p, Tin (*bcur)[kStageMax], Tin (*ccur)[kStageMax]) {
         const int ci = p / kPairs, n0 = 2 * (p - ci * kPairs);
         if (n0 == 0) {
             // new chunk: this lane's run of delta and u
@@ -386,26 +394,19 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         float Pex0, Hex0, Pex1, Hex1;
         state_phase1<T>(Arow[n0], dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0,
                         xagg[p & 1][0], lane, wv);
-        // second half of the previous step's window: C of pair p (already
-        // issued) and the rest of B of pair p + 1
-        if (p >= 1 && p + 1 < npairs) stage(Bb, p + 1, 1, bprev[1]);
         state_phase1<T>(Arow[n0 + 1], dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1,
                         xagg[p & 1][1], lane, wv);
-        wait_vmem();
         __syncthreads();
-        if (p + 1 < npairs) stage(Cb, p + 1, 0, cnxt[0]);
         state_phase2<T, kMaxWv>(a0, bu0, Pex0, Hex0, &ccur[0][run], yv, xagg[p & 1][0],
                                 hcar[wv][n0], lane, g, w, Wv);
-        if (p + 1 < npairs) stage(Cb, p + 1, 1, cnxt[1]);
-        if (p + 2 < npairs) stage(Bb, p + 2, 0, bcur[0]);
         state_phase2<T, kMaxWv>(a1, bu1, Pex1, Hex1, &ccur[1][run], yv, xagg[p & 1][1],
                                 hcar[wv][n0 + 1], lane, g, w, Wv);
         if (n0 + 2 == N && d_ok && cnt > 0) store_run<T>(yrow + t0, yv, full, cnt);
     };
 
     for (int p = 0; p < npairs; p += 2) {
-        pair_step(p, bst0, bst1, cst0, cst1);
-        if (p + 1 < npairs) pair_step(p + 1, bst1, bst0, cst1, cst0);
+        pair_step(p, bst0, cst0);
+        if (p + 1 < npairs) pair_step(p + 1, bst1, cst1);
     }
 }
 
@@ -420,11 +421,11 @@ vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y) {
     // runs of 13 positions; waves per channel from L
     constexpr int T = 13;
     const int Wv = L > 2 * kWave * T ? 4 : (L > kWave * T ? 2 : 1);
-    const int G = Wv == 4 ? 3 : (Wv == 2 ? 6 : 12);  // channels per workgroup: 12 waves
+    const int G = kComputeWaves / Wv;  // channels per workgroup
     const int n_groups = int((a.channels + G - 1) / G);
     const long long n_wg = static_cast<long long>(n_groups) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
-    const dim3 grid(static_cast<unsigned>(n_wg)), block(kWave * G * Wv);
+    const dim3 grid(static_cast<unsigned>(n_wg)), block(kStageThreads);
     hipLaunchKernelGGL((k_full_scan_chunked<N, T, Tin, Tout, kTwoD>), grid, block, 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,

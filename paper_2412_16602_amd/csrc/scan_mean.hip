@@ -8,162 +8,293 @@
 //   r_mean[t]      = mean_d D[c] u_{d,t}             (skip term, reduced with the scan)
 // then one N-state recurrence per (batch, k) and the broadcast of its output.
 //
-// Three passes over chunks of kMeanChunk positions:
-//   1. reduce : lanes own positions, each of the 4 waves sums a fixed quarter
-//               of the channels (coalesced loads along t, channel parameters
-//               wave-uniform), the quarters are added in a fixed order; the
-//               reduced tile is written to the workspace together with each
-//               chunk's scan aggregate (prod Abar, local end state) from a
-//               wave-level inclusive scan of the (a, b) pairs;
-//   2. carry  : one lane per (batch, k, n) walks the chunk aggregates and
-//               stores each chunk's incoming state;
-//   3. finish : re-runs the chunk's wave-level scan from its incoming state,
-//               forms ytilde and broadcasts it to every channel (sequence
-//               layout) or stores it for the merge-and-broadcast pass (2-D).
-// The (a, b) combine is (a1, b1) then (a2, b2) -> (a1 a2, a2 b1 + b2).
+// Three passes over chunks of kMeanChunk (64) positions:
+//   1. reduce : a workgroup owns one chunk of one (batch, k); lanes own
+//               positions (coalesced loads along t), each of its 8 waves sums
+//               a fixed eighth of the channels (channel parameters are
+//               wave-uniform), and the eighths are added in a fixed order in
+//               LDS. Each state's chunk-local inclusive scan of the pairs
+//               (Abar_mean, B s_mean), composed with
+//               (a1, b1) then (a2, b2) -> (a1 a2, a2 b1 + b2), is stored per
+//               position together with r_mean, and the chunk's aggregate
+//               (its last position) is what the carry pass chains.
+//   2. carry  : one wave per (batch, k, n) scans the chunk aggregates across
+//               lanes (DPP) and stores the state entering each chunk.
+//   3. finish : h[n,t] = P[n,t] * carry[n] + H[n,t], ytilde = sum_n C h + r,
+//               broadcast to every channel (sequence layout) or stored for
+//               the merge-and-broadcast pass (2-D layout).
+// All sums run in a fixed order, so results are deterministic.
 #include "vmb_internal.h"
 
 namespace vmb {
 namespace {
 
+constexpr int kWave = 64;
 constexpr int kC = kMeanChunk;  // positions per chunk = lanes per wave
-constexpr int kWaves = 4;
+constexpr int kRedWaves = 16;   // channel split of the reduce pass
+constexpr int kUnroll = 4;      // channels per load group (two groups in flight)
+constexpr int kFinWaves = 4;    // waves of a finish workgroup
+constexpr int kParamFloats = 12288;  // LDS budget for a direction's A rows (48 KB)
+constexpr int kParamChannels = 2048; // LDS budget for its dt_bias / D (16 KB)
 
-// Inclusive scan over the 64 lanes of a wave of the (a, b) pairs, in lane
-// order: on return lane i holds the composition of lanes 0..i.
-__device__ __forceinline__ void wave_scan(float& a, float& b, int lane) {
-#pragma unroll
-    for (int off = 1; off < kC; off <<= 1) {
-        const float pa = __shfl_up(a, off, kC);
-        const float pb = __shfl_up(b, off, kC);
-        if (lane >= off) {
-            b = __builtin_fmaf(a, pb, b);
-            a = a * pa;
-        }
-    }
+// Inclusive scan over the 64 lanes of the (a, b) pairs, in lane order
+// (lanes without a partner are left unchanged: identity).
+__device__ __forceinline__ void wave_scan(float& a, float& b) {
+    asm("s_nop 1\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+        "s_nop 1\n"
+        : "+v"(b), "+v"(a));
 }
 
+// Workspace layout, per (batch, k) = bk, for L positions and nch chunks:
+//   scan[bk][n][t][2] : chunk-local inclusive (P, H) of state n at position t
+//   rmean[bk][t]      : r_mean
+//   agg[bk][c][n][2]  : chunk aggregates (copy of the last position's scan)
+//   carry[bk][c][n]   : state entering chunk c
+struct MeanWs {
+    float* scan;
+    float* rmean;
+    float* agg;
+    float* carry;
+    float* ytil;  // 2-D layout: ytilde[bk][t]
+};
+
 template <int N, typename Tin, bool kTwoD>
-__global__ __launch_bounds__(kC* kWaves) void k_mean_reduce(
+__global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
-    float* __restrict__ red, float* __restrict__ agg, int K, int Dc, int L, int H, int W,
-    int nchunks, int softplus) {
-    __shared__ float part[kWaves][N + 2][kC];
+    MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks, int softplus) {
+    __shared__ float part[kRedWaves][N + 2][kC];
+    // this direction's channel parameters: A rows, dt_bias, D (0 when absent)
+    __shared__ float prm_a[kParamFloats];
+    __shared__ float prm_bd[2 * kParamChannels];
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
-    const int lane = threadIdx.x % kC, wv = threadIdx.x / kC;
-    const int t = chunk * kC + lane;
-    const bool valid = t < L;
+    const int lane = threadIdx.x % kC;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
+    const int t = chunk * C + lane;
+    const bool valid = lane < C && t < L;
     const int tc = valid ? t : L - 1;  // clamped: every address below stays in bounds
     const size_t bk = static_cast<size_t>(b) * K + k;
     const bool sp = softplus != 0;
     const int src = kTwoD ? pixel_of(k, tc, H, W) : tc;
-
     float acc[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) acc[n] = 0.0f;
     float s = 0.0f, r = 0.0f;
-    const int d0 = (wv * Dc) / kWaves, d1 = ((wv + 1) * Dc) / kWaves;
-    for (int d = d0; d < d1; ++d) {
-        const int c = k * Dc + d;
-        const size_t row = (bk * Dc + d) * static_cast<size_t>(L);
-        const size_t urow = kTwoD ? (static_cast<size_t>(b) * Dc + d) * L : row;
-        const float dv = valid ? to_f32(delta[row + tc]) : 0.0f;
-        const float uv = valid ? to_f32(u[urow + src]) : 0.0f;
-        const float bias = dt_bias ? dt_bias[c] : 0.0f;
-        const float dl = timescale(dv + bias, sp);
-        const float dl2 = dl * kLog2e;
+    const int d0 = (wv * Dc) / kRedWaves, d1 = ((wv + 1) * Dc) / kRedWaves;
+    auto load_group = [&](int dd, float (&dv)[kUnroll], float (&uv)[kUnroll]) {
 #pragma unroll
-        for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * A[static_cast<size_t>(c) * N + n]);
-        s = __builtin_fmaf(dl, uv, s);
-        r = __builtin_fmaf(D ? D[c] : 0.0f, uv, r);
+        for (int j = 0; j < kUnroll; ++j) {
+            const int d = dd + j < d1 ? dd + j : d1 - 1;
+            const size_t row = (bk * Dc + d) * static_cast<size_t>(L);
+            const size_t urow = kTwoD ? (static_cast<size_t>(b) * Dc + d) * L : row;
+            dv[j] = to_f32(delta[row + tc]);
+            uv[j] = to_f32(u[urow + src]);
+        }
+    };
+
+    // channel parameters: global loads first (so waiting for them does not
+    // wait for the delta / u stream issued after them), stored to LDS below
+    const bool in_lds = Dc * N <= kParamFloats && Dc <= kParamChannels;
+    constexpr int kPrmPer = (kParamFloats + kC * kRedWaves - 1) / (kC * kRedWaves);
+    float pa[kPrmPer];
+    if (in_lds) {
+        const float* Ak = A + static_cast<size_t>(k) * Dc * N;
+#pragma unroll
+        for (int q = 0; q < kPrmPer; ++q) {
+            const int i = threadIdx.x + q * kC * kRedWaves;
+            pa[q] = i < Dc * N ? Ak[i] : 0.0f;
+        }
+    }
+    // delta / u of the first three channel groups in flight (ring of four)
+    constexpr int kRing = 4;
+    float dv[kRing][kUnroll], uv[kRing][kUnroll];
+#pragma unroll
+    for (int g = 0; g < kRing - 1; ++g)
+        if (d0 + g * kUnroll < d1) load_group(d0 + g * kUnroll, dv[g], uv[g]);
+    if (in_lds) {
+#pragma unroll
+        for (int q = 0; q < kPrmPer; ++q) {
+            const int i = threadIdx.x + q * kC * kRedWaves;
+            if (i < Dc * N) prm_a[i] = pa[q];
+        }
+        for (int i = threadIdx.x; i < Dc; i += kC * kRedWaves) {
+            prm_bd[2 * i] = dt_bias ? dt_bias[k * Dc + i] : 0.0f;
+            prm_bd[2 * i + 1] = D ? D[k * Dc + i] : 0.0f;
+        }
+    }
+    __syncthreads();
+
+    for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
+#pragma unroll
+        for (int g = 0; g < kRing; ++g) {
+            const int gd = dd + g * kUnroll;
+            if (gd >= d1) break;
+            // keep three groups ahead in flight
+            const int pf = gd + (kRing - 1) * kUnroll;
+            if (pf < d1) load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
+#pragma unroll
+            for (int j = 0; j < kUnroll; ++j) {
+                if (gd + j >= d1) break;
+                const int dch = gd + j;
+                const int c = k * Dc + dch;
+                float bias, dskip;
+                const float* Ac;
+                if (in_lds) {
+                    bias = prm_bd[2 * dch];
+                    dskip = prm_bd[2 * dch + 1];
+                    Ac = prm_a + dch * N;
+                } else {
+                    bias = dt_bias ? dt_bias[c] : 0.0f;
+                    dskip = D ? D[c] : 0.0f;
+                    Ac = A + static_cast<size_t>(c) * N;
+                }
+                const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
+                const float dl2 = dl * kLog2e;
+#pragma unroll
+                for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * Ac[n]);
+                s = __builtin_fmaf(dl, uv[g][j], s);
+                r = __builtin_fmaf(dskip, uv[g][j], r);
+            }
+        }
     }
 #pragma unroll
     for (int n = 0; n < N; ++n) part[wv][n][lane] = acc[n];
     part[wv][N][lane] = s;
     part[wv][N + 1][lane] = r;
     __syncthreads();
-    if (wv != 0) return;
 
+    // channel groups added in a fixed order; wave w then scans states
+    // w, w + 16, ... of this chunk
     const float inv = 1.0f / static_cast<float>(Dc);
-    float* redbk = red + bk * (N + 2) * L;
     float sm = 0.0f;
-    for (int w = 0; w < kWaves; ++w) sm += part[w][N][lane];
+    for (int w = 0; w < kRedWaves; ++w) sm += part[w][N][lane];
     sm *= inv;
-    float rm = 0.0f;
-    for (int w = 0; w < kWaves; ++w) rm += part[w][N + 1][lane];
-    rm *= inv;
-    if (valid) {
-        redbk[static_cast<size_t>(N) * L + t] = sm;
-        redbk[static_cast<size_t>(N + 1) * L + t] = rm;
+    if (wv == 0) {
+        float rm = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) rm += part[w][N + 1][lane];
+        if (valid) ws.rmean[bk * L + t] = rm * inv;
     }
-    float* aggc = agg + (bk * nchunks + chunk) * N * 2;
-#pragma unroll
-    for (int n = 0; n < N; ++n) {
+    float* scan_bk = ws.scan + bk * N * L * 2;
+    float* agg_c = ws.agg + (bk * nchunks + chunk) * N * 2;
+    for (int n = wv; n < N; n += kRedWaves) {
         float am = 0.0f;
-        for (int w = 0; w < kWaves; ++w) am += part[w][n][lane];
+        for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
         am *= inv;
-        if (valid) redbk[static_cast<size_t>(n) * L + t] = am;
+        // positions past the end act as the identity (1, 0)
         float a = valid ? am : 1.0f;
         float bb = valid ? to_f32(Bm[(bk * N + n) * L + tc]) * sm : 0.0f;
-        wave_scan(a, bb, lane);
+        wave_scan(a, bb);
+        if (valid) {
+            float2 v = make_float2(a, bb);
+            *reinterpret_cast<float2*>(scan_bk + (static_cast<size_t>(n) * L + t) * 2) = v;
+        }
         if (lane == kC - 1) {
-            aggc[2 * n] = a;
-            aggc[2 * n + 1] = bb;
+            agg_c[2 * n] = a;
+            agg_c[2 * n + 1] = bb;
         }
     }
 }
 
-__global__ __launch_bounds__(64) void k_mean_carry(const float* __restrict__ agg,
-                                                   float* __restrict__ carry, int lanes, int N,
-                                                   int nchunks) {
-    const int i = blockIdx.x * 64 + threadIdx.x;
-    if (i >= lanes) return;
-    const size_t bk = i / N;
-    const int n = i - static_cast<int>(bk) * N;
-    float h = 0.0f;
-    for (int c = 0; c < nchunks; ++c) {
-        const size_t o = (bk * nchunks + c) * N + n;
-        carry[o] = h;
-        h = __builtin_fmaf(agg[2 * o], h, agg[2 * o + 1]);
+// One wave per (batch, k, n): exclusive scan of the chunk aggregates.
+__global__ __launch_bounds__(kWave) void k_mean_carry(MeanWs ws, int N, int nchunks) {
+    const int lane = threadIdx.x;
+    const size_t bk = blockIdx.x / N;
+    const int n = blockIdx.x % N;
+    float carry = 0.0f;  // state entering the current block of 64 chunks
+    for (int c0 = 0; c0 < nchunks; c0 += kWave) {
+        const int c = c0 + lane;
+        float a = 1.0f, bb = 0.0f;
+        if (c < nchunks) {
+            const size_t o = ((bk * nchunks + c) * N + n) * 2;
+            a = ws.agg[o];
+            bb = ws.agg[o + 1];
+        }
+        wave_scan(a, bb);
+        // state entering chunk c = carry composed with the chunks before c
+        const float pa = __shfl_up(a, 1, kWave), pb = __shfl_up(bb, 1, kWave);
+        const float cin = lane == 0 ? carry : __builtin_fmaf(pa, carry, pb);
+        if (c < nchunks) ws.carry[(bk * nchunks + c) * N + n] = cin;
+        const float la = __shfl(a, kWave - 1, kWave), lb = __shfl(bb, kWave - 1, kWave);
+        carry = __builtin_fmaf(la, carry, lb);
     }
 }
 
+// grid: (block of 64 positions, k * groups, batch). Wave w forms the C h
+// contribution of states w, w + 4, ... for the block's positions (each lane
+// taking the state entering its own chunk), the four partials and r_mean are
+// added in a fixed order, and every wave writes its share of the group's
+// channels. With at most 64 chunks per sequence the entering states come
+// from an exclusive scan of the chunk aggregates done here (lanes = chunks);
+// otherwise from the carry pass.
 template <int N, typename Tin, typename Tout, bool kTwoD>
-__global__ __launch_bounds__(kC* kWaves) void k_mean_finish(
-    const float* __restrict__ red, const float* __restrict__ carry, const Tin* __restrict__ Bm,
-    const Tin* __restrict__ Cm, Tout* __restrict__ y, float* __restrict__ ytil, int K, int Dc,
-    int L, int nchunks) {
-    __shared__ float ybuf[kC];
-    const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
-    const int lane = threadIdx.x % kC, wv = threadIdx.x / kC;
-    const int t = chunk * kC + lane;
+__global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish(MeanWs ws, const Tin* __restrict__ Cm,
+                                                             Tout* __restrict__ y, int K, int Dc,
+                                                             int L, int C, int nchunks, int groups,
+                                                             int inline_carry) {
+    __shared__ float part[kFinWaves][kC];
+    const int blk = blockIdx.x, k = blockIdx.y / groups, grp = blockIdx.y % groups;
+    const int b = blockIdx.z;
+    const int lane = threadIdx.x % kC;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
+    const int t = blk * kC + lane;
     const bool valid = t < L;
-    const int tc = valid ? t : L - 1;  // clamped: every address below stays in bounds
+    const int tc = valid ? t : L - 1;
+    const int ch = tc / C;  // chunk of this position
     const size_t bk = static_cast<size_t>(b) * K + k;
-    if (wv == 0) {
-        const float* redbk = red + bk * (N + 2) * L;
-        const float* carc = carry + (bk * nchunks + chunk) * N;
-        const float sm = valid ? redbk[static_cast<size_t>(N) * L + tc] : 0.0f;
-        float acc = valid ? redbk[static_cast<size_t>(N + 1) * L + tc] : 0.0f;
-#pragma unroll
-        for (int n = 0; n < N; ++n) {
-            float a = valid ? redbk[static_cast<size_t>(n) * L + tc] : 1.0f;
-            float bb = valid ? to_f32(Bm[(bk * N + n) * L + tc]) * sm : 0.0f;
-            wave_scan(a, bb, lane);
-            const float h = __builtin_fmaf(a, carc[n], bb);
-            const float cv = valid ? to_f32(Cm[(bk * N + n) * L + tc]) : 0.0f;
-            acc = __builtin_fmaf(cv, h, acc);
+    const float* scan_bk = ws.scan + bk * N * L * 2;
+    float acc = 0.0f;
+    for (int n = wv; n < N; n += kFinWaves) {
+        float cin;
+        if (inline_carry) {
+            // lanes = chunks: inclusive scan of the aggregates, then the
+            // value of lane ch - 1 is the state entering chunk ch
+            float a = 1.0f, bb = 0.0f;
+            if (lane < nchunks) {
+                const size_t o = ((bk * nchunks + lane) * N + n) * 2;
+                a = ws.agg[o];
+                bb = ws.agg[o + 1];
+            }
+            wave_scan(a, bb);
+            const float prev = __shfl(bb, ch > 0 ? ch - 1 : 0, kWave);
+            cin = ch > 0 ? prev : 0.0f;
+        } else {
+            cin = ws.carry[(bk * nchunks + ch) * N + n];
         }
-        ybuf[lane] = acc;
-        if (kTwoD && valid) ytil[bk * L + t] = acc;
+        const float2 ph =
+            *reinterpret_cast<const float2*>(scan_bk + (static_cast<size_t>(n) * L + tc) * 2);
+        const float h = __builtin_fmaf(ph.x, cin, ph.y);
+        acc = __builtin_fmaf(to_f32(Cm[(bk * N + n) * L + tc]), h, acc);
     }
-    if (kTwoD) return;
+    part[wv][lane] = acc;
     __syncthreads();
     if (!valid) return;
-    const float v = ybuf[lane];
-    const Tout o = from_f32<Tout>(v);
-    for (int d = wv; d < Dc; d += kWaves) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
+    float yt = ws.rmean[bk * L + tc];
+#pragma unroll
+    for (int w = 0; w < kFinWaves; ++w) yt += part[w][lane];
+    if constexpr (kTwoD) {
+        if (wv == 0 && grp == 0) ws.ytil[bk * L + t] = yt;
+        return;
+    }
+    const Tout o = from_f32<Tout>(yt);
+    const int dg0 = (grp * Dc) / groups, dg1 = ((grp + 1) * Dc) / groups;
+    for (int d = dg0 + wv; d < dg1; d += kFinWaves) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
 }
 
 // 2-D layout: fold the four reduced sequences of each batch element into one
@@ -188,39 +319,45 @@ __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __res
 
 template <int N, typename Tin, typename Tout, bool kTwoD>
 vmb_status run(const ScanArgs& a) {
-    const int nchunks = static_cast<int>((a.L + kC - 1) / kC);
     const size_t bkn = static_cast<size_t>(a.batch * a.K);
-    auto round_up = [](size_t v) { return (v + 255) & ~size_t{255}; };
-    char* ws = static_cast<char*>(a.ws);
-    float* red = reinterpret_cast<float*>(ws);
-    ws += round_up(bkn * (N + 2) * a.L * 4);
-    float* agg = reinterpret_cast<float*>(ws);
-    ws += round_up(bkn * nchunks * N * 2 * 4);
-    float* carry = reinterpret_cast<float*>(ws);
-    ws += round_up(bkn * nchunks * N * 4);
-    float* ytil = kTwoD ? reinterpret_cast<float*>(ws) : nullptr;
+    const MeanWsLayout lay = mean_ws_layout(a.batch, a.K, a.L, N, kTwoD);
+    char* p = static_cast<char*>(a.ws);
+    MeanWs ws;
+    ws.scan = reinterpret_cast<float*>(p + lay.scan);
+    ws.rmean = reinterpret_cast<float*>(p + lay.rmean);
+    ws.agg = reinterpret_cast<float*>(p + lay.agg);
+    ws.carry = reinterpret_cast<float*>(p + lay.carry);
+    ws.ytil = kTwoD ? reinterpret_cast<float*>(p + lay.ytil) : nullptr;
 
-    const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
-    const dim3 block(kC * kWaves);
     const int K = int(a.K), Dc = int(a.channels), L = int(a.L), H = int(a.H), W = int(a.W);
-    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD>), grid, block, 0, a.stream,
+    const int C = mean_chunk(a.batch, a.K, a.L);
+    const int nchunks = (L + C - 1) / C;
+    const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
+    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD>), grid, dim3(kC * kRedWaves), 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
-                       static_cast<const Tin*>(a.B), a.D, a.dt_bias, red, agg, K, Dc, L, H, W,
+                       static_cast<const Tin*>(a.B), a.D, a.dt_bias, ws, K, Dc, L, H, W, C,
                        nchunks, a.softplus);
     vmb_status st = check_launch();
     if (st != VMB_OK) return st;
-    const int lanes = static_cast<int>(bkn * N);
-    hipLaunchKernelGGL(k_mean_carry, dim3((lanes + 63) / 64), dim3(64), 0, a.stream, agg, carry,
-                       lanes, N, nchunks);
-    st = check_launch();
-    if (st != VMB_OK) return st;
-    hipLaunchKernelGGL((k_mean_finish<N, Tin, Tout, kTwoD>), grid, block, 0, a.stream, red, carry,
-                       static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C),
-                       static_cast<Tout*>(a.y), ytil, K, Dc, L, nchunks);
+    const int inline_carry = nchunks <= kWave ? 1 : 0;
+    if (!inline_carry) {
+        hipLaunchKernelGGL(k_mean_carry, dim3(static_cast<unsigned>(bkn * N)), dim3(kWave), 0,
+                           a.stream, ws, N, nchunks);
+        st = check_launch();
+        if (st != VMB_OK) return st;
+    }
+    // channel groups of the finish pass spread the broadcast stores over more
+    // workgroups (2-D layout: one group, it stores the reduced sequence)
+    const int groups = kTwoD ? 1 : (Dc >= 64 ? 4 : 1);
+    const int nblk = (L + kC - 1) / kC;
+    hipLaunchKernelGGL((k_mean_finish<N, Tin, Tout, kTwoD>),
+                       dim3(nblk, static_cast<unsigned>(a.K * groups), unsigned(a.batch)),
+                       dim3(kC * kFinWaves), 0, a.stream, ws, static_cast<const Tin*>(a.C),
+                       static_cast<Tout*>(a.y), K, Dc, L, C, nchunks, groups, inline_carry);
     st = check_launch();
     if (st != VMB_OK || !kTwoD) return st;
     hipLaunchKernelGGL(k_mean_merge_broadcast<Tout>, dim3((L + 255) / 256, unsigned(a.batch)),
-                       dim3(256), 0, a.stream, ytil, static_cast<Tout*>(a.y), Dc, H, W);
+                       dim3(256), 0, a.stream, ws.ytil, static_cast<Tout*>(a.y), Dc, H, W);
     return check_launch();
 }
 

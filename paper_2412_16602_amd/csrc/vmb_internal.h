@@ -42,6 +42,52 @@ size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t 
 // Chunk length (positions) of the mean variant's reduce / carry / finish passes.
 constexpr int kMeanChunk = 64;
 
+// Positions per chunk of the mean variant (at most kMeanChunk): the number of
+// chunks over all (batch, direction) sequences is rounded towards a multiple
+// of 256 workgroups (the compute units of one MI355X) where that wastes few
+// lanes, e.g. 49 positions (256 workgroups) for 4 x 3136.
+inline int mean_chunk(int64_t batch, int64_t K, int64_t L) {
+    const int64_t seqs = batch * K;
+    int best = kMeanChunk;
+    double best_cost = 1e300;
+    for (int c = 32; c <= kMeanChunk; ++c) {
+        const int64_t wgs = seqs * ((L + c - 1) / c);
+        const int64_t rounds = (wgs + 255) / 256;
+        // ~ time per CU: rounds of workgroups, each a fixed overhead plus c positions
+        const double cost = static_cast<double>(rounds) * (c + 16);
+        if (cost < best_cost - 1e-9) {
+            best_cost = cost;
+            best = c;
+        }
+    }
+    return best;
+}
+
+// Byte offsets of the mean variant's workspace regions (each 256-byte
+// aligned), for bk = batch * K direction sequences of L positions:
+//   scan  [bk][N][L][2] float : chunk-local inclusive scan (P, H)
+//   rmean [bk][L]       float : channel mean of D * u
+//   agg   [bk][nch][N][2]     : chunk aggregates
+//   carry [bk][nch][N]        : state entering each chunk
+//   ytil  [bk][L]             : 2-D layout only, the reduced output
+struct MeanWsLayout {
+    size_t scan, rmean, agg, carry, ytil, total;
+};
+inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t L, int64_t N, bool two_d) {
+    auto up = [](size_t v) { return (v + 255) & ~size_t{255}; };
+    const size_t bk = static_cast<size_t>(batch) * static_cast<size_t>(K);
+    const int chunk = mean_chunk(batch, K, L);
+    const size_t nch = static_cast<size_t>((L + chunk - 1) / chunk);
+    MeanWsLayout o;
+    o.scan = 0;
+    o.rmean = o.scan + up(bk * N * L * 2 * 4);
+    o.agg = o.rmean + up(bk * L * 4);
+    o.carry = o.agg + up(bk * nch * N * 2 * 4);
+    o.ytil = o.carry + up(bk * nch * N * 4);
+    o.total = o.ytil + (two_d ? up(bk * L * 4) : 0);
+    return o;
+}
+
 // Launchers (enqueue only; arguments already validated).
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
                              int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);

@@ -72,13 +72,7 @@ size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t 
         // 2-D layout: per-direction fp32 outputs, folded by the merge pass
         return layout == VMB_LAYOUT_2D ? round_up(static_cast<size_t>(seq) * 4) : 0;
     }
-    const int64_t nchunks = (L + kMeanChunk - 1) / kMeanChunk;
-    size_t bytes = 0;
-    bytes += round_up(static_cast<size_t>(batch * K * (N + 2) * L) * 4);       // reduced tile
-    bytes += round_up(static_cast<size_t>(batch * K * nchunks * N) * 2 * 4);   // chunk aggregates
-    bytes += round_up(static_cast<size_t>(batch * K * nchunks * N) * 4);       // chunk carries
-    if (layout == VMB_LAYOUT_2D) bytes += round_up(static_cast<size_t>(batch * K * L) * 4);
-    return bytes;
+    return mean_ws_layout(batch, K, L, N, layout == VMB_LAYOUT_2D).total;
 }
 
 vmb_status validate_scan(const ScanArgs& a, int mean_variant) {

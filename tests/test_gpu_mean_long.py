@@ -1,0 +1,31 @@
+"""VMeanba scan on long sequences: many chunks (separate carry pass), chunk
+boundaries that do not align with the 64-position finish blocks, 2-D layout."""
+import pytest
+
+import workloads
+from gpu_util import FP32_TOL, assert_close, log, oracle_seq, run_scan, to_f64
+from test_gpu_scan import merged_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("L,channels,batch", [(2049, 8, 1), (3136, 5, 1), (4097, 3, 2),
+                                              (8193, 4, 1), (65536, 2, 1)])
+def test_mean_long(L, channels, batch):
+    log(f"mean long L={L} channels={channels} batch={batch}")
+    shp = workloads.custom_shape(batch, 1, L, channels, 16, "f32", L + channels, True)
+    inp = workloads.make_inputs(shp, "seq", d_value=0.0)
+    got = to_f64(run_scan(inp, "mean", "seq"))
+    ref = oracle_seq(inp, "mean", "seq")
+    assert_close(got, ref, **FP32_TOL, what=f"mean L={L}")
+
+
+@pytest.mark.parametrize("H,W", [(64, 130), (56, 56)])
+def test_mean_2d_long(H, W):
+    log(f"mean 2d {H}x{W}")
+    shp = workloads.custom_shape(1, H, W, 6, 16, "f32", H + W, True)
+    inp = workloads.make_inputs(shp, "2d")
+    got = to_f64(run_scan(inp, "mean", "2d"))
+    ref, scale = merged_oracle(inp, "mean")
+    assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
+                 what=f"mean 2d {H}x{W}")
