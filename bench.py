@@ -15,7 +15,17 @@ Cache), so every step streams from HBM.
 
 Prints one JSON line (rank 0). The `roofline` object covers the dominant
 kernel, the full scan, timed alone on the sequence layout with HIP events on
-its stream; `cpu_baseline` times the fp64 oracle on the host.
+its stream. Its arithmetic floor (one exp and five other VALU slots per
+(channel, state, position)) lies above its HBM floor, so it is reported as
+ALU-bound: 7 FLOP per element against the 45.9 TFLOP/s this instruction mix
+can reach (256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz non-packed fp32 issue, exp at
+half rate); the HBM fraction is reported next to it. `traffic` is the HBM
+bytes per launch measured with rocprofv3 counters (profiles/), reported only
+while the kernel source still matches the one profiled. `cpu_baseline` times
+the fp64 oracle on the host.
+
+--calibrate runs a plain 256 MiB device copy first, the reference dispatch the
+counter runs scale FETCH_SIZE / WRITE_SIZE by.
 """
 from __future__ import annotations
 
@@ -34,6 +44,16 @@ if ROOT not in sys.path:
 import workloads  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
+# non-packed fp32 VALU issue: 256 CUs * 4 SIMDs * 16 lanes * 2.4 GHz lane-slots/s
+VALU_SLOTS_PER_S = 256 * 4 * 16 * 2.4e9
+# per (channel, state, position): Delta*A, exp, Delta*u*B, state FMA, output FMA
+FLOP_PER_ELEM = 7
+SLOTS_PER_ELEM = 6  # mul, exp (2 slots: half-rate transcendental), mul, fma, fma
+ALU_PEAK_TFLOPS = VALU_SLOTS_PER_S * FLOP_PER_ELEM / SLOTS_PER_ELEM / 1e12
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "full_scan_seq_56x56_c192_n16_traffic.txt")
+# the sources the profiled kernel is compiled from
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2412_16602_amd", "csrc", f)
+                  for f in ("scan_chunked.hip", "vmb_internal.h")]
 METRIC = ("SS2D selective-scan µs/call + HBM GB/s (% peak), full vs mean, "
           "VMamba-T 56×56")
 ROTATE_BYTES = 768 << 20  # > 2x the 256 MB MALL
@@ -135,6 +155,44 @@ def gpu_bench(args):
     return res, step_bytes, scan_bytes, n_rot
 
 
+def source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the full scan from the committed counter summary
+    (lines "key: value"), or None if absent or taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            kv = dict(line.split(":", 1) for line in f if ":" in line)
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("kernel_sources_sha256_16") != source_hash():
+        return None
+    try:
+        return int(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def calibrate_copy():
+    """A plain streaming kernel of known size: 256 MiB read, 256 MiB written
+    (an elementwise negation, so it shows up as its own kernel)."""
+    import torch
+    src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def cpu_baseline(budget_s: float):
     """The fp64 oracle on the host: one SS2D forward (cross-scan, full scan,
     merge) at the bench workload, repeated until about budget_s seconds."""
@@ -167,17 +225,24 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="run a 256 MiB copy first (counter calibration dispatch)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this SS2D scan library runs on a single "
               "MI355X and has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
+    if args.calibrate:
+        calibrate_copy()
     res, step_bytes, scan_bytes, n_rot = gpu_bench(args)
     full, mean = res["ss2d_full"], res["ss2d_mean"]
     sfull, smean = res["seq_full"], res["seq_mean"]
     kern_us = sfull["us"]
     achieved = scan_bytes / (kern_us * 1e-6) / 1e9
+    shp = workloads.STAGE1
+    elems = shp.batch * 4 * shp.channels * shp.N * shp.L
+    achieved_tf = elems * FLOP_PER_ELEM / (kern_us * 1e-6) / 1e12
     out = {
         "metric": METRIC,
         "value": round(full["us"], 3),
@@ -205,10 +270,15 @@ def main():
                      "full_gbps": round(scan_bytes / (sfull["us"] * 1e-6) / 1e9, 1),
                      "mean_gbps": round(scan_bytes / (smean["us"] * 1e-6) / 1e9, 1),
                      "mean_speedup": round(sfull["us"] / smean["us"], 3)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "kernel": "full scan, sequence layout",
-                     "algorithmic_bytes": scan_bytes, "avg_us": round(kern_us, 3)},
+        "roofline": {"bound": "alu", "achieved": round(achieved_tf, 3),
+                     "peak": round(ALU_PEAK_TFLOPS, 2), "unit": "TFLOP/s",
+                     "frac": round(achieved_tf / ALU_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(),
+                     "kernel": "full scan (positions over lanes), sequence layout",
+                     "avg_us": round(kern_us, 3), "elements": elems,
+                     "flop_per_element": FLOP_PER_ELEM,
+                     "algorithmic_bytes": scan_bytes, "hbm_gbps": round(achieved, 1),
+                     "hbm_frac": round(achieved / HBM_PEAK_GBPS, 4)},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
