@@ -190,40 +190,36 @@ __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], co
 }
 
 // Phase 2 (after the workgroup barrier): state entering this wave from the
-// channel's earlier waves and the previous chunk, then the re-walk of the run
-// from the state entering this lane, accumulating y_i += C_i h_i. All waves
-// of a channel compose the same aggregates in the same order, so the state
-// carried to the next chunk is identical in each of them.
-template <int T, int kMaxWv, typename Tin>
+// channel's earlier waves and the previous chunk (*hcar, this wave's own copy
+// of the carry), then the re-walk of the run from the state entering this
+// lane, accumulating y_i += C_i h_i. Every wave of a channel composes the same
+// aggregates in the same order, so every copy of the carry into the next chunk
+// (the state leaving the channel's last wave) is the same.
+template <int T, int kWv, typename Tin>
 __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pex,
                                              float Hex, const Tin* csrc, float (&yv)[T],
-                                             const float (*xg)[2], float& hc, int lane, int g,
-                                             int w, int Wv) {
-    float xp[kMaxWv], xh[kMaxWv];
-#pragma unroll
-    for (int j = 0; j < kMaxWv; ++j) {
-        if (j < Wv) {
-            xp[j] = xg[g * Wv + j][0];
-            xh[j] = xg[g * Wv + j][1];
-        }
-    }
+                                             const float (*xg)[2], float* hcar, int lane, int g,
+                                             int w) {
+    const float hc = *hcar;
     float cin = hc;
-    float cnext = cin;
+    float cnext = hc;
 #pragma unroll
-    for (int j = 0; j < kMaxWv; ++j) {
-        if (j < Wv) {
-            cnext = __builtin_fmaf(xp[j], cnext, xh[j]);
-            if (j + 1 == w) cin = cnext;
-        }
+    for (int j = 0; j < kWv; ++j) {
+        const float2 x = *reinterpret_cast<const float2*>(xg[g * kWv + j]);
+        cnext = __builtin_fmaf(x.x, cnext, x.y);
+        if (j + 1 < kWv && j + 1 == w) cin = cnext;
     }
-    if (w == 0) cin = hc;
-    if (lane == 0) hc = cnext;
     float h = __builtin_fmaf(Pex, cin, Hex);
 #pragma unroll
     for (int i = 0; i < T; ++i) {
         h = __builtin_fmaf(a[i], h, bu[i]);
         yv[i] = __builtin_fmaf(to_f32(csrc[i]), h, yv[i]);
     }
+    // finish the re-walk here: left to itself the compiler sinks it past the
+    // next step's phase 1, which then needs two steps' run arrays at once
+#pragma unroll
+    for (int i = 0; i < T; ++i) asm volatile("" : "+v"(yv[i]));
+    if (lane == 0) *hcar = cnext;
 }
 
 // Slice of the B or C row of one state copied into LDS: positions
@@ -275,18 +271,20 @@ __device__ __forceinline__ void stage_one(const Tin* base, int p, int s, Tin* ds
 // LDS copies above) are done: vmcnt(0), other counters untouched.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
-template <int N, int T, typename Tin, typename Tout, bool kTwoD>
+template <int N, int T, int kWv, typename Tin, typename Tout, bool kTwoD>
 __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
     const float* __restrict__ dt_bias, Tout* __restrict__ y, int K, int Dc, int L, int H, int W,
-    int softplus, int G, int Wv, int n_groups, int n_wg) {
-    static_assert(N % 2 == 0, "states are processed in pairs");
-    constexpr int kMaxWv = 4;
+    int softplus, int n_groups, int n_wg) {
+    static_assert(N % 4 == 0, "states go in pairs, and pairs alternate stage buffers");
+    static_assert(kComputeWaves % kWv == 0, "whole channels per workgroup");
     constexpr int kPairs = N / 2;
+    constexpr int G = kComputeWaves / kWv;  // channels per workgroup
     // per (parity, state of the pair, wave): aggregates exchanged across waves
-    __shared__ float xagg[2][2][16][2];
-    __shared__ float hcar[16][N];
+    __shared__ __align__(16) float xagg[2][2][kComputeWaves][2];
+    __shared__ __align__(16) float arow[G][N];  // A rows of the workgroup's channels
+    __shared__ float hcar[kComputeWaves][N];    // per wave: state carried into the next chunk
     // B and C slices of a pair of states, double-buffered (distinct arrays so
     // that copies into one buffer never order reads of the other)
     __shared__ Tin bst0[2][kStageMax], bst1[2][kStageMax];
@@ -305,9 +303,8 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
-    const int chunk = Wv * kWave * T;
+    const int chunk = kWv * kWave * T;
     const int nchunks = (L + chunk - 1) / chunk;
-    const int npairs = nchunks * kPairs;  // step = (chunk, pair of states)
     const bool vec4 = (L % (16 / static_cast<int>(sizeof(Tin)))) == 0;
     const Tin* Bb = Bm + static_cast<size_t>(bk) * N * L;
     const Tin* Cb = Cm + static_cast<size_t>(bk) * N * L;
@@ -316,6 +313,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         // Copy waves. Before barrier p they issue C of pair p and B of pair
         // p + 1, into buffers last read before barrier p - 1, then wait for
         // their completion; barrier p publishes them.
+        const int npairs = nchunks * kPairs;  // step = (chunk, pair of states)
         const int issuer = wv - kComputeWaves;
         auto stage = [&](const Tin* base, int p, int st, Tin* dst) {
             stage_one<kPairs>(base, p, st, dst, L, chunk, vec4, issuer, lane);
@@ -339,7 +337,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         return;
     }
 
-    const int g = wv / Wv, w = wv - g * Wv;
+    const int g = wv / kWv, w = wv - g * kWv;
     const int d_raw = dg * G + g;
     const bool d_ok = d_raw < Dc;
     const int d = d_ok ? d_raw : Dc - 1;
@@ -351,62 +349,68 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const float bias = dt_bias ? dt_bias[c] : 0.0f;
     const float dskip = D ? D[c] : 0.0f;
     const bool sp = softplus != 0;
-    const float* Arow = A + static_cast<size_t>(c) * N;
+    if (w == 0)
+        for (int n = lane; n < N; n += kWave) arow[g][n] = A[static_cast<size_t>(c) * N + n];
+    for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
     const int run = (w * kWave + lane) * T;  // this lane's first position inside a chunk
 
-    for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
-    __syncthreads();
+    __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
+    const float* an = arow[g];
 
-    float dl2[T], du[T], yv[T];
-    float s2 = 0.0f;
-    int t0 = 0, cnt = 0;
-    bool full = false;
-
-    // One pair step: phase 1 reads B of the pair (published by the previous
-    // barrier), the barrier publishes this step's wave aggregates and C of
-    // the pair, phase 2 reads them.
-    auto pair_step = [&](int p, Tin (*bcur)[kStageMax], Tin (*ccur)[kStageMax]) {
-        const int ci = p / kPairs, n0 = 2 * (p - ci * kPairs);
-        if (n0 == 0) {
-            // new chunk: this lane's run of delta and u
-            t0 = ci * chunk + run;
-            cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
-            full = cnt == T;
-            const int tl = cnt > 0 ? t0 : 0;  // keep addresses in range for empty runs
+    for (int ci = 0; ci < nchunks; ++ci) {
+        // this lane's run of delta and u
+        const int t0 = ci * chunk + run;
+        const int cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
+        const bool full = cnt == T;
+        const int tl = cnt > 0 ? t0 : 0;  // keep addresses in range for empty runs
+        float dl2[T], du[T], yv[T];
+        float s2 = 0.0f;
+        {
             float dv[T], uv[T];
             load_run<T>(drow + tl, dv, full, cnt);
             if constexpr (kTwoD)
                 load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
             else
                 load_run<T>(urow + tl, uv, full, cnt);
-            s2 = 0.0f;
+            if (sp) {
+#pragma unroll
+                for (int i = 0; i < T; ++i) dv[i] = timescale(dv[i] + bias, true);
+            } else {
+#pragma unroll
+                for (int i = 0; i < T; ++i) dv[i] += bias;
+            }
 #pragma unroll
             for (int i = 0; i < T; ++i) {
                 // positions past the end act as the identity: a = 1, b = 0
-                const float dl = i < cnt ? timescale(dv[i] + bias, sp) : 0.0f;
+                const float dl = (full || i < cnt) ? dv[i] : 0.0f;
                 dl2[i] = dl * kLog2e;
                 du[i] = dl * uv[i];
                 yv[i] = dskip * uv[i];
                 s2 += dl2[i];
             }
         }
-        float a0[T], bu0[T], a1[T], bu1[T];
-        float Pex0, Hex0, Pex1, Hex1;
-        state_phase1<T>(Arow[n0], dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0,
-                        xagg[p & 1][0], lane, wv);
-        state_phase1<T>(Arow[n0 + 1], dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1,
-                        xagg[p & 1][1], lane, wv);
-        __syncthreads();
-        state_phase2<T, kMaxWv>(a0, bu0, Pex0, Hex0, &ccur[0][run], yv, xagg[p & 1][0],
-                                hcar[wv][n0], lane, g, w, Wv);
-        state_phase2<T, kMaxWv>(a1, bu1, Pex1, Hex1, &ccur[1][run], yv, xagg[p & 1][1],
-                                hcar[wv][n0 + 1], lane, g, w, Wv);
-        if (n0 + 2 == N && d_ok && cnt > 0) store_run<T>(yrow + t0, yv, full, cnt);
-    };
-
-    for (int p = 0; p < npairs; p += 2) {
-        pair_step(p, bst0, cst0);
-        if (p + 1 < npairs) pair_step(p + 1, bst1, cst1);
+        // One pair step per barrier: phase 1 reads B of the pair (published
+        // by the previous barrier), the barrier publishes the wave aggregates
+        // and C of the pair, phase 2 reads them.
+        auto pair_step = [&](int n0, Tin (*bcur)[kStageMax], Tin (*ccur)[kStageMax],
+                             float (*xq)[kComputeWaves][2]) {
+            const float2 a01 = *reinterpret_cast<const float2*>(an + n0);
+            float a0[T], bu0[T], a1[T], bu1[T];
+            float Pex0, Hex0, Pex1, Hex1;
+            state_phase1<T>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0, xq[0], lane, wv);
+            state_phase1<T>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1, xq[1], lane, wv);
+            __syncthreads();
+            state_phase2<T, kWv>(a0, bu0, Pex0, Hex0, &ccur[0][run], yv, xq[0], &hcar[wv][n0], lane,
+                                 g, w);
+            state_phase2<T, kWv>(a1, bu1, Pex1, Hex1, &ccur[1][run], yv, xq[1], &hcar[wv][n0 + 1],
+                                 lane, g, w);
+        };
+#pragma unroll 1
+        for (int q = 0; q < kPairs; q += 2) {
+            pair_step(2 * q, bst0, cst0, xagg[0]);
+            pair_step(2 * q + 2, bst1, cst1, xagg[1]);
+        }
+        if (d_ok && cnt > 0) store_run<T>(yrow + t0, yv, full, cnt);
     }
 }
 
@@ -414,24 +418,30 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
 
 // Chunked full scan: picks the run length and waves per channel from L.
 namespace {
-template <int N, typename Tin, typename Tout, bool kTwoD>
-vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y) {
-    const int L = int(a.L);
-    // waves per channel and run length: cover L with few idle lanes
-    // runs of 13 positions; waves per channel from L
-    constexpr int T = 13;
-    const int Wv = L > 2 * kWave * T ? 4 : (L > kWave * T ? 2 : 1);
-    const int G = kComputeWaves / Wv;  // channels per workgroup
+template <int N, int kWv, typename Tin, typename Tout, bool kTwoD>
+vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y) {
+    constexpr int T = 13;  // positions per lane run
+    constexpr int G = kComputeWaves / kWv;  // channels per workgroup
     const int n_groups = int((a.channels + G - 1) / G);
     const long long n_wg = static_cast<long long>(n_groups) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
     const dim3 grid(static_cast<unsigned>(n_wg)), block(kStageThreads);
-    hipLaunchKernelGGL((k_full_scan_chunked<N, T, Tin, Tout, kTwoD>), grid, block, 0, a.stream,
+    hipLaunchKernelGGL((k_full_scan_chunked<N, T, kWv, Tin, Tout, kTwoD>), grid, block, 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,
-                       y, int(a.K), int(a.channels), L, int(a.H), int(a.W), a.softplus, G, Wv,
+                       y, int(a.K), int(a.channels), int(a.L), int(a.H), int(a.W), a.softplus,
                        n_groups, int(n_wg));
     return check_launch();
+}
+
+// Waves per channel from L: cover the sequence in one chunk where possible
+// (runs of 13 positions, 64 lanes per wave).
+template <int N, typename Tin, typename Tout, bool kTwoD>
+vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y) {
+    const int64_t L = a.L;
+    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD>(a, y);
+    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD>(a, y);
+    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD>(a, y);
 }
 }  // namespace
 
