@@ -354,24 +354,27 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
     const int run = (w * kWave + lane) * T;  // this lane's first position inside a chunk
 
-    __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
+    // This lane's run of delta and u for chunk ci; chunk 0's loads are issued
+    // before the first barrier so that they overlap the first B copy.
+    auto load_chunk = [&](int ci, float (&dv)[T], float (&uv)[T]) {
+        const int t0 = ci * chunk + run;
+        const int cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
+        const int tl = cnt > 0 ? t0 : 0;  // keep addresses in range for empty runs
+        load_run<T>(drow + tl, dv, cnt == T, cnt);
+        if constexpr (kTwoD)
+            load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
+        else
+            load_run<T>(urow + tl, uv, cnt == T, cnt);
+    };
     const float* an = arow[g];
-
-    for (int ci = 0; ci < nchunks; ++ci) {
-        // this lane's run of delta and u
+    // One chunk, from this lane's delta / u run (dv, uv) to the stored y run.
+    auto chunk_body = [&](int ci, float (&dv)[T], float (&uv)[T]) __attribute__((always_inline)) {
         const int t0 = ci * chunk + run;
         const int cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
         const bool full = cnt == T;
-        const int tl = cnt > 0 ? t0 : 0;  // keep addresses in range for empty runs
         float dl2[T], du[T], yv[T];
         float s2 = 0.0f;
         {
-            float dv[T], uv[T];
-            load_run<T>(drow + tl, dv, full, cnt);
-            if constexpr (kTwoD)
-                load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
-            else
-                load_run<T>(urow + tl, uv, full, cnt);
             if (sp) {
 #pragma unroll
                 for (int i = 0; i < T; ++i) dv[i] = timescale(dv[i] + bias, true);
@@ -411,6 +414,22 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
             pair_step(2 * q + 2, bst1, cst1, xagg[1]);
         }
         if (d_ok && cnt > 0) store_run<T>(yrow + t0, yv, full, cnt);
+    };
+
+    float dv0[T], uv0[T];
+    load_chunk(0, dv0, uv0);
+
+    __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
+    // keep every use of the loaded values after the barrier (the compiler
+    // would otherwise wait for the loads before it)
+#pragma unroll
+    for (int i = 0; i < T; ++i) asm volatile("" : "+v"(dv0[i]), "+v"(uv0[i]));
+
+    chunk_body(0, dv0, uv0);
+    for (int ci = 1; ci < nchunks; ++ci) {
+        float dv[T], uv[T];
+        load_chunk(ci, dv, uv);
+        chunk_body(ci, dv, uv);
     }
 }
 
