@@ -116,23 +116,45 @@ __device__ __forceinline__ void load_run(const bf16_t* p, float (&v)[T], bool fu
     }
 }
 
+// Stores one wave's outputs: lane l holds the run of T values at positions
+// seg0 + l*T .. seg0 + l*T + T - 1 (nval valid positions in all). Written
+// straight from the runs, each store instruction would touch every lane's
+// own cache lines; instead the wave passes the values through its own LDS
+// slice (stride T words: no bank conflicts) and stores them lane-contiguous,
+// 4 values per lane (aligned rows) or 1.
 template <int T, typename Tout>
-__device__ __forceinline__ void store_run(Tout* p, const float (&v)[T], bool full, int cnt) {
-    if constexpr (sizeof(Tout) == 4) {
-        if (full) {
+__device__ __forceinline__ void store_wave(Tout* dst, const float (&v)[T], float* slice, int lane,
+                                           int nval, bool aligned4) {
 #pragma unroll
-            for (int i = 0; i + 4 <= T; i += 4) {
-                const float4 q = make_float4(v[i], v[i + 1], v[i + 2], v[i + 3]);
-                __builtin_memcpy(p + i, &q, 16);
+    for (int i = 0; i < T; ++i) slice[lane * T + i] = v[i];
+    if (aligned4) {
+        constexpr int kQuads = (kWave * T) / 4;
+#pragma unroll
+        for (int j0 = 0; j0 < kQuads; j0 += kWave) {
+            const int j = j0 + lane;
+            if (j < kQuads && 4 * j < nval) {
+                const float4 q = *reinterpret_cast<const float4*>(slice + 4 * j);
+                if (4 * j + 4 <= nval) {
+                    if constexpr (sizeof(Tout) == 4) {
+                        *reinterpret_cast<float4*>(dst + 4 * j) = q;
+                    } else {
+                        Tout o[4] = {from_f32<Tout>(q.x), from_f32<Tout>(q.y), from_f32<Tout>(q.z),
+                                     from_f32<Tout>(q.w)};
+                        __builtin_memcpy(dst + 4 * j, o, sizeof(o));
+                    }
+                } else {
+                    const float e[4] = {q.x, q.y, q.z, q.w};
+                    for (int r = 0; r < nval - 4 * j; ++r) dst[4 * j + r] = from_f32<Tout>(e[r]);
+                }
             }
+        }
+    } else {
 #pragma unroll
-            for (int i = T & ~3; i < T; ++i) p[i] = v[i];
-            return;
+        for (int i = 0; i < T; ++i) {
+            const int j = i * kWave + lane;
+            if (j < nval) dst[j] = from_f32<Tout>(slice[j]);
         }
     }
-#pragma unroll
-    for (int i = 0; i < T; ++i)
-        if (full || i < cnt) p[i] = from_f32<Tout>(v[i]);
 }
 
 // u values of a run in the 2-D layout: position t of direction k reads pixel
@@ -289,6 +311,8 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     // that copies into one buffer never order reads of the other)
     __shared__ Tin bst0[2][kStageMax], bst1[2][kStageMax];
     __shared__ Tin cst0[2][kStageMax], cst1[2][kStageMax];
+    // per compute wave: its outputs on their way to a coalesced store
+    __shared__ __align__(16) float ystage[kComputeWaves][kWave * T];
 
     // XCD-aware numbering: hardware places workgroup i on XCD i % 8
     const int bid = blockIdx.x;
@@ -413,7 +437,10 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
             pair_step(2 * q, bst0, cst0, xagg[0]);
             pair_step(2 * q + 2, bst1, cst1, xagg[1]);
         }
-        if (d_ok && cnt > 0) store_run<T>(yrow + t0, yv, full, cnt);
+        const int seg0 = ci * chunk + w * kWave * T;  // this wave's first position
+        if (d_ok && seg0 < L)
+            store_wave<T>(yrow + seg0, yv, ystage[wv], lane, min(kWave * T, L - seg0),
+                          (L & 3) == 0);
     };
 
     float dv0[T], uv0[T];
