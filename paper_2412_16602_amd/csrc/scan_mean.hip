@@ -141,38 +141,51 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     }
     __syncthreads();
 
-    for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
+    // The channel loop, instantiated once with the parameters in LDS and once
+    // reading them from global memory, so that each copy addresses its
+    // parameters directly (not through generic pointers that would wait on
+    // the delta / u stream).
+    auto channels = [&](auto params) {
+        for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
 #pragma unroll
-        for (int g = 0; g < kRing; ++g) {
-            const int gd = dd + g * kUnroll;
-            if (gd >= d1) break;
-            // keep three groups ahead in flight
-            const int pf = gd + (kRing - 1) * kUnroll;
-            if (pf < d1) load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
+            for (int g = 0; g < kRing; ++g) {
+                const int gd = dd + g * kUnroll;
+                if (gd >= d1) break;
+                // keep three groups ahead in flight
+                const int pf = gd + (kRing - 1) * kUnroll;
+                if (pf < d1)
+                    load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
 #pragma unroll
-            for (int j = 0; j < kUnroll; ++j) {
-                if (gd + j >= d1) break;
-                const int dch = gd + j;
-                const int c = k * Dc + dch;
-                float bias, dskip;
-                const float* Ac;
-                if (in_lds) {
-                    bias = prm_bd[2 * dch];
-                    dskip = prm_bd[2 * dch + 1];
-                    Ac = prm_a + dch * N;
-                } else {
-                    bias = dt_bias ? dt_bias[c] : 0.0f;
-                    dskip = D ? D[c] : 0.0f;
-                    Ac = A + static_cast<size_t>(c) * N;
+                for (int j = 0; j < kUnroll; ++j) {
+                    if (gd + j >= d1) break;
+                    const int dch = gd + j;
+                    float bias, dskip, an[N];
+                    params(dch, bias, dskip, an);
+                    const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
+                    const float dl2 = dl * kLog2e;
+#pragma unroll
+                    for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * an[n]);
+                    s = __builtin_fmaf(dl, uv[g][j], s);
+                    r = __builtin_fmaf(dskip, uv[g][j], r);
                 }
-                const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
-                const float dl2 = dl * kLog2e;
-#pragma unroll
-                for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * Ac[n]);
-                s = __builtin_fmaf(dl, uv[g][j], s);
-                r = __builtin_fmaf(dskip, uv[g][j], r);
             }
         }
+    };
+    if (in_lds) {
+        channels([&](int dch, float& bias, float& dskip, float (&an)[N]) {
+            bias = prm_bd[2 * dch];
+            dskip = prm_bd[2 * dch + 1];
+#pragma unroll
+            for (int n = 0; n < N; ++n) an[n] = prm_a[dch * N + n];
+        });
+    } else {
+        channels([&](int dch, float& bias, float& dskip, float (&an)[N]) {
+            const int c = k * Dc + dch;
+            bias = dt_bias ? dt_bias[c] : 0.0f;
+            dskip = D ? D[c] : 0.0f;
+#pragma unroll
+            for (int n = 0; n < N; ++n) an[n] = A[static_cast<size_t>(c) * N + n];
+        });
     }
 #pragma unroll
     for (int n = 0; n < N; ++n) part[wv][n][lane] = acc[n];
