@@ -34,8 +34,6 @@ constexpr int kC = kMeanChunk;  // positions per chunk = lanes per wave
 constexpr int kRedWaves = 16;   // channel split of the reduce pass
 constexpr int kUnroll = 4;      // channels per load group (two groups in flight)
 constexpr int kFinWaves = 4;    // waves of a finish workgroup
-constexpr int kParamFloats = 12288;  // LDS budget for a direction's A rows (48 KB)
-constexpr int kParamChannels = 2048; // LDS budget for its dt_bias / D (16 KB)
 
 // Inclusive scan over the 64 lanes of the (a, b) pairs, in lane order
 // (lanes without a partner are left unchanged: identity).
@@ -81,9 +79,6 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
     MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks, int softplus) {
     __shared__ float part[kRedWaves][N + 2][kC];
-    // this direction's channel parameters: A rows, dt_bias, D (0 when absent)
-    __shared__ float prm_a[kParamFloats];
-    __shared__ float prm_bd[2 * kParamChannels];
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
@@ -109,83 +104,36 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
         }
     };
 
-    // channel parameters: global loads first (so waiting for them does not
-    // wait for the delta / u stream issued after them), stored to LDS below
-    const bool in_lds = Dc * N <= kParamFloats && Dc <= kParamChannels;
-    constexpr int kPrmPer = (kParamFloats + kC * kRedWaves - 1) / (kC * kRedWaves);
-    float pa[kPrmPer];
-    if (in_lds) {
-        const float* Ak = A + static_cast<size_t>(k) * Dc * N;
-#pragma unroll
-        for (int q = 0; q < kPrmPer; ++q) {
-            const int i = threadIdx.x + q * kC * kRedWaves;
-            pa[q] = i < Dc * N ? Ak[i] : 0.0f;
-        }
-    }
     // delta / u of the first three channel groups in flight (ring of four)
     constexpr int kRing = 4;
     float dv[kRing][kUnroll], uv[kRing][kUnroll];
 #pragma unroll
     for (int g = 0; g < kRing - 1; ++g)
         if (d0 + g * kUnroll < d1) load_group(d0 + g * kUnroll, dv[g], uv[g]);
-    if (in_lds) {
+    // Channel parameters are wave-uniform: scalar loads, no staging.
+    for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
 #pragma unroll
-        for (int q = 0; q < kPrmPer; ++q) {
-            const int i = threadIdx.x + q * kC * kRedWaves;
-            if (i < Dc * N) prm_a[i] = pa[q];
-        }
-        for (int i = threadIdx.x; i < Dc; i += kC * kRedWaves) {
-            prm_bd[2 * i] = dt_bias ? dt_bias[k * Dc + i] : 0.0f;
-            prm_bd[2 * i + 1] = D ? D[k * Dc + i] : 0.0f;
-        }
-    }
-    __syncthreads();
-
-    // The channel loop, instantiated once with the parameters in LDS and once
-    // reading them from global memory, so that each copy addresses its
-    // parameters directly (not through generic pointers that would wait on
-    // the delta / u stream).
-    auto channels = [&](auto params) {
-        for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
+        for (int g = 0; g < kRing; ++g) {
+            const int gd = dd + g * kUnroll;
+            if (gd >= d1) break;
+            // keep three groups ahead in flight
+            const int pf = gd + (kRing - 1) * kUnroll;
+            if (pf < d1) load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
 #pragma unroll
-            for (int g = 0; g < kRing; ++g) {
-                const int gd = dd + g * kUnroll;
-                if (gd >= d1) break;
-                // keep three groups ahead in flight
-                const int pf = gd + (kRing - 1) * kUnroll;
-                if (pf < d1)
-                    load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
+            for (int j = 0; j < kUnroll; ++j) {
+                if (gd + j >= d1) break;
+                const int c = k * Dc + gd + j;
+                const float bias = dt_bias ? dt_bias[c] : 0.0f;
+                const float dskip = D ? D[c] : 0.0f;
+                const float* Ac = A + static_cast<size_t>(c) * N;
+                const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
+                const float dl2 = dl * kLog2e;
 #pragma unroll
-                for (int j = 0; j < kUnroll; ++j) {
-                    if (gd + j >= d1) break;
-                    const int dch = gd + j;
-                    float bias, dskip, an[N];
-                    params(dch, bias, dskip, an);
-                    const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
-                    const float dl2 = dl * kLog2e;
-#pragma unroll
-                    for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * an[n]);
-                    s = __builtin_fmaf(dl, uv[g][j], s);
-                    r = __builtin_fmaf(dskip, uv[g][j], r);
-                }
+                for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * Ac[n]);
+                s = __builtin_fmaf(dl, uv[g][j], s);
+                r = __builtin_fmaf(dskip, uv[g][j], r);
             }
         }
-    };
-    if (in_lds) {
-        channels([&](int dch, float& bias, float& dskip, float (&an)[N]) {
-            bias = prm_bd[2 * dch];
-            dskip = prm_bd[2 * dch + 1];
-#pragma unroll
-            for (int n = 0; n < N; ++n) an[n] = prm_a[dch * N + n];
-        });
-    } else {
-        channels([&](int dch, float& bias, float& dskip, float (&an)[N]) {
-            const int c = k * Dc + dch;
-            bias = dt_bias ? dt_bias[c] : 0.0f;
-            dskip = D ? D[c] : 0.0f;
-#pragma unroll
-            for (int n = 0; n < N; ++n) an[n] = A[static_cast<size_t>(c) * N + n];
-        });
     }
 #pragma unroll
     for (int n = 0; n < N; ++n) part[wv][n][lane] = acc[n];
