@@ -70,7 +70,7 @@ struct MeanWs {
     float* rmean;
     float* agg;
     float* carry;
-    float* ytil;  // 2-D layout: ytilde[bk][t]
+    float* ytil;  // 2-D layout: reduced output ytilde[bk][t]
 };
 
 template <int N, typename Tin, bool kTwoD>
@@ -197,18 +197,76 @@ __global__ __launch_bounds__(kWave) void k_mean_carry(MeanWs ws, int N, int nchu
     }
 }
 
-// grid: (block of 64 positions, k * groups, batch). Wave w forms the C h
-// contribution of states w, w + 4, ... for the block's positions (each lane
-// taking the state entering its own chunk), the four partials and r_mean are
-// added in a fixed order, and every wave writes its share of the group's
-// channels. With at most 64 chunks per sequence the entering states come
-// from an exclusive scan of the chunk aggregates done here (lanes = chunks);
-// otherwise from the carry pass.
+// C h summed over the states n = wv, wv + kFinWaves, ... of each of kDirs
+// sequences bk[i] at positions t[i] (chunk-local scan composed with the state
+// entering the position's chunk). The entering state comes, with at most 64
+// chunks per sequence, from an exclusive scan of the chunk aggregates done
+// here (lanes = chunks, then lane ch - 1's inclusive value), otherwise from
+// the carry pass. All loads are issued before any of the scans.
+template <int N, int kDirs, typename Tin>
+__device__ __forceinline__ void ch_partials(const MeanWs& ws, const Tin* __restrict__ Cm,
+                                            const size_t (&bk)[kDirs], int L, const int (&t)[kDirs],
+                                            int C, int nchunks, bool inline_carry, int lane,
+                                            int wv, float (&acc)[kDirs]) {
+    constexpr int kPer = N / kFinWaves > 0 ? N / kFinWaves : 1;
+    float ga[kDirs][kPer], gb[kDirs][kPer], cv[kDirs][kPer];
+    float2 ph[kDirs][kPer];
+#pragma unroll
+    for (int i = 0; i < kDirs; ++i) {
+        const float* scan_bk = ws.scan + bk[i] * N * L * 2;
+        const int ch = t[i] / C;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int n = wv + j * kFinWaves;
+            const bool on = n < N;
+            const int nn = on ? n : 0;
+            ga[i][j] = 1.0f;
+            gb[i][j] = 0.0f;
+            if (inline_carry) {
+                if (on && lane < nchunks) {
+                    const size_t o = ((bk[i] * nchunks + lane) * N + nn) * 2;
+                    ga[i][j] = ws.agg[o];
+                    gb[i][j] = ws.agg[o + 1];
+                }
+            } else {
+                gb[i][j] = ws.carry[(bk[i] * nchunks + ch) * N + nn];
+            }
+            ph[i][j] = *reinterpret_cast<const float2*>(scan_bk +
+                                                        (static_cast<size_t>(nn) * L + t[i]) * 2);
+            cv[i][j] = on ? to_f32(Cm[(bk[i] * N + nn) * L + t[i]]) : 0.0f;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kDirs; ++i) {
+        const int ch = t[i] / C;
+        acc[i] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            float cin = gb[i][j];
+            if (inline_carry) {
+                float a = ga[i][j], bb = gb[i][j];
+                wave_scan(a, bb);
+                const float prev = __shfl(bb, ch > 0 ? ch - 1 : 0, kWave);
+                cin = ch > 0 ? prev : 0.0f;
+            }
+            const float h = __builtin_fmaf(ph[i][j].x, cin, ph[i][j].y);
+            acc[i] = __builtin_fmaf(cv[i][j], h, acc[i]);
+        }
+    }
+}
+
+// Sequence layout. grid: (block of 64 positions, k * groups, batch). The
+// four waves form the C h partials of their states, the partials and r_mean
+// are added in a fixed order, and every wave writes its share of the group's
+// channels (lane-contiguous rows).
+// With kTwoD the reduced sequence itself is stored (to ws.ytil) for the
+// merge-and-broadcast pass.
 template <int N, typename Tin, typename Tout, bool kTwoD>
-__global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish(MeanWs ws, const Tin* __restrict__ Cm,
-                                                             Tout* __restrict__ y, int K, int Dc,
-                                                             int L, int C, int nchunks, int groups,
-                                                             int inline_carry) {
+__global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(MeanWs ws,
+                                                                 const Tin* __restrict__ Cm,
+                                                                 Tout* __restrict__ y, int K,
+                                                                 int Dc, int L, int C, int nchunks,
+                                                                 int groups, int inline_carry) {
     __shared__ float part[kFinWaves][kC];
     const int blk = blockIdx.x, k = blockIdx.y / groups, grp = blockIdx.y % groups;
     const int b = blockIdx.z;
@@ -217,40 +275,19 @@ __global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish(MeanWs ws, const 
     const int t = blk * kC + lane;
     const bool valid = t < L;
     const int tc = valid ? t : L - 1;
-    const int ch = tc / C;  // chunk of this position
     const size_t bk = static_cast<size_t>(b) * K + k;
-    const float* scan_bk = ws.scan + bk * N * L * 2;
-    float acc = 0.0f;
-    for (int n = wv; n < N; n += kFinWaves) {
-        float cin;
-        if (inline_carry) {
-            // lanes = chunks: inclusive scan of the aggregates, then the
-            // value of lane ch - 1 is the state entering chunk ch
-            float a = 1.0f, bb = 0.0f;
-            if (lane < nchunks) {
-                const size_t o = ((bk * nchunks + lane) * N + n) * 2;
-                a = ws.agg[o];
-                bb = ws.agg[o + 1];
-            }
-            wave_scan(a, bb);
-            const float prev = __shfl(bb, ch > 0 ? ch - 1 : 0, kWave);
-            cin = ch > 0 ? prev : 0.0f;
-        } else {
-            cin = ws.carry[(bk * nchunks + ch) * N + n];
-        }
-        const float2 ph =
-            *reinterpret_cast<const float2*>(scan_bk + (static_cast<size_t>(n) * L + tc) * 2);
-        const float h = __builtin_fmaf(ph.x, cin, ph.y);
-        acc = __builtin_fmaf(to_f32(Cm[(bk * N + n) * L + tc]), h, acc);
-    }
-    part[wv][lane] = acc;
+    const size_t bks[1] = {bk};
+    const int ts[1] = {tc};
+    float acc[1];
+    ch_partials<N, 1>(ws, Cm, bks, L, ts, C, nchunks, inline_carry != 0, lane, wv, acc);
+    part[wv][lane] = acc[0];
     __syncthreads();
     if (!valid) return;
     float yt = ws.rmean[bk * L + tc];
 #pragma unroll
     for (int w = 0; w < kFinWaves; ++w) yt += part[w][lane];
     if constexpr (kTwoD) {
-        if (wv == 0 && grp == 0) ws.ytil[bk * L + t] = yt;
+        if (wv == 0) ws.ytil[bk * L + t] = yt;
         return;
     }
     const Tout o = from_f32<Tout>(yt);
@@ -259,14 +296,16 @@ __global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish(MeanWs ws, const 
 }
 
 // 2-D layout: fold the four reduced sequences of each batch element into one
-// map, (y0 + y2) + (y1 + y3) per pixel, and broadcast it to every channel.
+// map, (y0 + y2) + (y1 + y3) per pixel (the cross-merge, same association as
+// the standalone merge), and broadcast it to the channels of group blockIdx.y.
+// grid: (block of 256 pixels, channel groups, batch).
 template <typename Tout>
 __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __restrict__ ytil,
                                                               Tout* __restrict__ y, int Dc, int H,
-                                                              int W) {
+                                                              int W, int groups) {
     const int L = H * W;
     const int p = blockIdx.x * 256 + threadIdx.x;
-    const int b = blockIdx.y;
+    const int grp = blockIdx.y, b = blockIdx.z;
     if (p >= L) return;
     const int hh = p / W, ww = p - hh * W;
     const int q = ww * H + hh;
@@ -274,8 +313,16 @@ __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __res
     const float s02 = yb[p] + yb[2 * static_cast<size_t>(L) + (L - 1 - p)];
     const float s13 = yb[static_cast<size_t>(L) + q] + yb[3 * static_cast<size_t>(L) + (L - 1 - q)];
     const Tout o = from_f32<Tout>(s02 + s13);
+    const int dg0 = (grp * Dc) / groups, dg1 = ((grp + 1) * Dc) / groups;
     Tout* yp = y + static_cast<size_t>(b) * Dc * L + p;
-    for (int d = 0; d < Dc; ++d) yp[static_cast<size_t>(d) * L] = o;
+    for (int d = dg0; d < dg1; ++d) yp[static_cast<size_t>(d) * L] = o;
+}
+
+// Channel groups for a broadcast pass: the wanted count, at least 1 and at
+// most one group per 16 channels.
+inline int clamp_groups(long long want, int Dc) {
+    const long long most = Dc >= 16 ? Dc / 16 : 1;
+    return static_cast<int>(want < 1 ? 1 : (want > most ? most : want));
 }
 
 template <int N, typename Tin, typename Tout, bool kTwoD>
@@ -307,18 +354,26 @@ vmb_status run(const ScanArgs& a) {
         st = check_launch();
         if (st != VMB_OK) return st;
     }
-    // channel groups of the finish pass spread the broadcast stores over more
-    // workgroups (2-D layout: one group, it stores the reduced sequence)
-    const int groups = kTwoD ? 1 : (Dc >= 64 ? 4 : 1);
+    // channel groups of the finish pass: enough workgroups to spread the
+    // broadcast stores (each group recomputes the reduced output it stores);
+    // the 2-D layout stores the reduced sequences once and broadcasts them in
+    // the merge pass
     const int nblk = (L + kC - 1) / kC;
-    hipLaunchKernelGGL((k_mean_finish<N, Tin, Tout, kTwoD>),
+    const long long seqs = a.batch * a.K;
+    const long long want = (512 + nblk * seqs - 1) / (nblk * seqs);
+    const int groups = kTwoD ? 1 : clamp_groups(want, Dc);
+    hipLaunchKernelGGL((k_mean_finish_seq<N, Tin, Tout, kTwoD>),
                        dim3(nblk, static_cast<unsigned>(a.K * groups), unsigned(a.batch)),
                        dim3(kC * kFinWaves), 0, a.stream, ws, static_cast<const Tin*>(a.C),
                        static_cast<Tout*>(a.y), K, Dc, L, C, nchunks, groups, inline_carry);
     st = check_launch();
     if (st != VMB_OK || !kTwoD) return st;
-    hipLaunchKernelGGL(k_mean_merge_broadcast<Tout>, dim3((L + 255) / 256, unsigned(a.batch)),
-                       dim3(256), 0, a.stream, ws.ytil, static_cast<Tout*>(a.y), Dc, H, W);
+    const int pblk = (L + 255) / 256;
+    const long long mwant = (512 + pblk * a.batch - 1) / (pblk * a.batch);
+    const int mgroups = clamp_groups(mwant, Dc);
+    hipLaunchKernelGGL(k_mean_merge_broadcast<Tout>,
+                       dim3(pblk, static_cast<unsigned>(mgroups), unsigned(a.batch)), dim3(256), 0,
+                       a.stream, ws.ytil, static_cast<Tout*>(a.y), Dc, H, W, mgroups);
     return check_launch();
 }
 
