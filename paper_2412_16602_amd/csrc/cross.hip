@@ -5,11 +5,13 @@
 // folds four sequences back into one map. Direction maps, pixel p = h*W + w:
 //   pi_0 = p, pi_1 = w*H + h, pi_2 = L-1-pi_0, pi_3 = L-1-pi_1.
 //
-// Both kernels move a 32 x 32 pixel tile of one (batch, channel) plane per
-// workgroup. The row-major directions are read / written along w; the
-// column-major ones need the transposed tile, which goes through LDS so that
-// every global access stays coalesced (consecutive lanes touch consecutive
-// addresses, ascending for directions 0/1 and descending for 2/3).
+// Planes that fit in LDS (the feature maps of VMamba's stages) are moved by
+// one workgroup each, 16 bytes per lane: directions 0 and 2 (and the merge's
+// own row order) straight between registers and memory, directions 1 and 3
+// through a padded copy of the plane in LDS (row stride W + 1 words, so the
+// column walk is free of bank conflicts). Every global access is a full
+// 16-byte vector of consecutive elements. Larger planes use 32 x 32 pixel
+// tiles (blockDim 32 x 8) with an LDS transpose for the column directions.
 #include "vmb_internal.h"
 
 namespace vmb {
@@ -100,6 +102,150 @@ __global__ __launch_bounds__(kTile* kRows) void k_cross_merge(const Tin* __restr
     }
 }
 
+// ---- whole-plane kernels (one workgroup per (batch, channel) plane)
+
+constexpr int kPlaneThreads = 768;
+constexpr int kPlaneLdsWords = 12288;  // padded plane H * (W + 1) fp32 words (48 KB)
+
+template <typename T, int V>
+struct Vec {
+    T v[V];
+};
+
+// Whole vectors at their natural alignment (callers guarantee it).
+template <typename T, int V>
+__device__ __forceinline__ Vec<T, V> load_vec(const T* p) {
+    Vec<T, V> r;
+    __builtin_memcpy(&r, __builtin_assume_aligned(p, sizeof(r)), sizeof(r));
+    return r;
+}
+
+template <typename T, int V>
+__device__ __forceinline__ void store_vec(T* p, const Vec<T, V>& r) {
+    __builtin_memcpy(__builtin_assume_aligned(p, sizeof(r)), &r, sizeof(r));
+}
+
+// V elements per lane; L % V == 0 and 16-byte aligned planes when V > 1.
+template <typename T, int V>
+__global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __restrict__ x,
+                                                                    T* __restrict__ xs, int Dc,
+                                                                    int H, int W) {
+    __shared__ T tile[kPlaneLdsWords];
+    const int L = H * W, Wp = W + 1;
+    const int plane = blockIdx.x;  // b * Dc + d
+    const int b = plane / Dc;
+    const int d = plane - b * Dc;
+    const T* src = x + static_cast<size_t>(plane) * L;
+    const size_t seq = static_cast<size_t>(L);
+    T* out0 = xs + (static_cast<size_t>(b) * 4 * Dc + d) * seq;
+    T* out1 = out0 + static_cast<size_t>(Dc) * seq;
+    T* out2 = out1 + static_cast<size_t>(Dc) * seq;
+    T* out3 = out2 + static_cast<size_t>(Dc) * seq;
+    const int nv = L / V;
+    // every load of this lane issued first (one memory round trip), then
+    // directions 0 and 2 from registers and the plane parked (padded) for 1, 3
+    constexpr int kPer = (kPlaneLdsWords / V + kPlaneThreads - 1) / kPlaneThreads;
+    Vec<T, V> v[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int j = threadIdx.x + i * kPlaneThreads;
+        if (j < nv) v[i] = load_vec<T, V>(src + j * V);
+    }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int j = threadIdx.x + i * kPlaneThreads;
+        if (j >= nv) break;
+        const int p = j * V;
+        store_vec<T, V>(out0 + p, v[i]);
+        Vec<T, V> r;
+#pragma unroll
+        for (int e = 0; e < V; ++e) r.v[e] = v[i].v[V - 1 - e];
+        store_vec<T, V>(out2 + (L - V - p), r);
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            const int pe = p + e, h = pe / W, w = pe - h * W;
+            tile[h * Wp + w] = v[i].v[e];
+        }
+    }
+    __syncthreads();
+    // directions 1 and 3: position q = w * H + h reads pixel (h, w)
+    for (int j = threadIdx.x; j < nv; j += kPlaneThreads) {
+        const int q = j * V;
+        Vec<T, V> v, r;
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            const int qe = q + e, w = qe / H, h = qe - w * H;
+            v.v[e] = tile[h * Wp + w];
+            r.v[V - 1 - e] = v.v[e];
+        }
+        store_vec<T, V>(out1 + q, v);
+        store_vec<T, V>(out3 + (L - V - q), r);
+    }
+}
+
+template <typename Tin, typename Tout, int V>
+__global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* __restrict__ ys,
+                                                                     Tout* __restrict__ y, int Dc,
+                                                                     int H, int W) {
+    __shared__ float s13[kPlaneLdsWords];
+    const int L = H * W, Wp = W + 1;
+    const int plane = blockIdx.x;
+    const int b = plane / Dc;
+    const int d = plane - b * Dc;
+    const size_t seq = static_cast<size_t>(L);
+    const Tin* in0 = ys + (static_cast<size_t>(b) * 4 * Dc + d) * seq;
+    const Tin* in1 = in0 + static_cast<size_t>(Dc) * seq;
+    const Tin* in2 = in1 + static_cast<size_t>(Dc) * seq;
+    const Tin* in3 = in2 + static_cast<size_t>(Dc) * seq;
+    Tout* dst = y + static_cast<size_t>(plane) * L;
+    const int nv = L / V;
+    // every load of this lane issued first (one memory round trip)
+    constexpr int kPer = (kPlaneLdsWords / V + kPlaneThreads - 1) / kPlaneThreads;
+    Vec<Tin, V> a1[kPer], a3[kPer], a0[kPer], a2[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int j = threadIdx.x + i * kPlaneThreads;
+        if (j < nv) {
+            const int o = j * V;
+            a1[i] = load_vec<Tin, V>(in1 + o);
+            a3[i] = load_vec<Tin, V>(in3 + (L - V - o));
+            a0[i] = load_vec<Tin, V>(in0 + o);
+            a2[i] = load_vec<Tin, V>(in2 + (L - V - o));
+        }
+    }
+    // y1 + y3 of each pixel, in column order (q = w * H + h), parked by pixel
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int j = threadIdx.x + i * kPlaneThreads;
+        if (j >= nv) break;
+        const int q = j * V;
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            const int qe = q + e, w = qe / H, h = qe - w * H;
+            s13[h * Wp + w] = to_f32(a1[i].v[e]) + to_f32(a3[i].v[V - 1 - e]);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int j = threadIdx.x + i * kPlaneThreads;
+        if (j >= nv) break;
+        const int p = j * V;
+        Vec<Tout, V> o;
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            const int pe = p + e, h = pe / W, w = pe - h * W;
+            const float s02 = to_f32(a0[i].v[e]) + to_f32(a2[i].v[V - 1 - e]);
+            o.v[e] = from_f32<Tout>(s02 + s13[h * Wp + w]);
+        }
+        store_vec<Tout, V>(dst + p, o);
+    }
+}
+
+bool plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
+    return H * (W + 1) <= kPlaneLdsWords && batch * channels <= 0x7fffffff;
+}
+
 // grid: x = plane (b * channels + d), y = tile row, z = tile column
 dim3 tile_grid(int64_t batch, int64_t channels, int64_t H, int64_t W) {
     return dim3(static_cast<unsigned>(batch * channels),
@@ -116,6 +262,27 @@ bool grid_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
 
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
                              int64_t H, int64_t W, vmb_dtype dt, hipStream_t s) {
+    if (plane_fits(batch, channels, H, W)) {
+        const dim3 grid(static_cast<unsigned>(batch * channels)), block(kPlaneThreads);
+        const int c = int(channels), h = int(H), w = int(W);
+        const int64_t L = H * W;
+        if (dt == VMB_F32) {
+            const float* xi = static_cast<const float*>(x);
+            float* xo = static_cast<float*>(xs);
+            if (L % 4 == 0)
+                hipLaunchKernelGGL((k_cross_scan_plane<float, 4>), grid, block, 0, s, xi, xo, c, h, w);
+            else
+                hipLaunchKernelGGL((k_cross_scan_plane<float, 1>), grid, block, 0, s, xi, xo, c, h, w);
+        } else {
+            const bf16_t* xi = static_cast<const bf16_t*>(x);
+            bf16_t* xo = static_cast<bf16_t*>(xs);
+            if (L % 8 == 0)
+                hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 8>), grid, block, 0, s, xi, xo, c, h, w);
+            else
+                hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 1>), grid, block, 0, s, xi, xo, c, h, w);
+        }
+        return check_launch();
+    }
     if (!grid_fits(batch, channels, H, W)) return VMB_ERR_UNSUPPORTED;
     const dim3 grid = tile_grid(batch, channels, H, W), block(kTile, kRows);
     if (dt == VMB_F32)
@@ -128,9 +295,35 @@ vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t cha
     return check_launch();
 }
 
+template <typename Tin, typename Tout>
+void launch_merge_plane(const void* ys, void* y, int64_t batch, int64_t channels, int64_t H,
+                        int64_t W, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>(batch * channels)), block(kPlaneThreads);
+    const int c = int(channels), h = int(H), w = int(W);
+    const Tin* in = static_cast<const Tin*>(ys);
+    Tout* out = static_cast<Tout*>(y);
+    // 16-byte vectors on both sides: 4 elements of the wider type
+    constexpr int V = (sizeof(Tin) == 2 && sizeof(Tout) == 2) ? 8 : 4;
+    if ((H * W) % V == 0)
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V>), grid, block, 0, s, in, out, c, h, w);
+    else
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, 1>), grid, block, 0, s, in, out, c, h, w);
+}
+
 vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t channels,
                               int64_t H, int64_t W, vmb_dtype in_dt, vmb_dtype out_dt,
                               hipStream_t s) {
+    if (plane_fits(batch, channels, H, W)) {
+        if (in_dt == VMB_F32 && out_dt == VMB_F32)
+            launch_merge_plane<float, float>(ys, y, batch, channels, H, W, s);
+        else if (in_dt == VMB_F32 && out_dt == VMB_BF16)
+            launch_merge_plane<float, bf16_t>(ys, y, batch, channels, H, W, s);
+        else if (in_dt == VMB_BF16 && out_dt == VMB_BF16)
+            launch_merge_plane<bf16_t, bf16_t>(ys, y, batch, channels, H, W, s);
+        else
+            return VMB_ERR_DTYPE;
+        return check_launch();
+    }
     if (!grid_fits(batch, channels, H, W)) return VMB_ERR_UNSUPPORTED;
     const dim3 grid = tile_grid(batch, channels, H, W), block(kTile, kRows);
     const int c = int(channels), h = int(H), w = int(W);
