@@ -126,7 +126,9 @@ __device__ __forceinline__ void store_vec(T* p, const Vec<T, V>& r) {
 }
 
 // V elements per lane; L % V == 0 and 16-byte aligned planes when V > 1.
-template <typename T, int V>
+// kAll = false writes only the column-major copy of each plane (direction 1's
+// sequence), to xs[plane][L].
+template <typename T, int V, bool kAll>
 __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __restrict__ x,
                                                                     T* __restrict__ xs, int Dc,
                                                                     int H, int W) {
@@ -138,7 +140,7 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
     const T* src = x + static_cast<size_t>(plane) * L;
     const size_t seq = static_cast<size_t>(L);
     T* out0 = xs + (static_cast<size_t>(b) * 4 * Dc + d) * seq;
-    T* out1 = out0 + static_cast<size_t>(Dc) * seq;
+    T* out1 = kAll ? out0 + static_cast<size_t>(Dc) * seq : xs + static_cast<size_t>(plane) * seq;
     T* out2 = out1 + static_cast<size_t>(Dc) * seq;
     T* out3 = out2 + static_cast<size_t>(Dc) * seq;
     const int nv = L / V;
@@ -156,11 +158,13 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
         const int j = threadIdx.x + i * kPlaneThreads;
         if (j >= nv) break;
         const int p = j * V;
-        store_vec<T, V>(out0 + p, v[i]);
-        Vec<T, V> r;
+        if constexpr (kAll) {
+            store_vec<T, V>(out0 + p, v[i]);
+            Vec<T, V> r;
 #pragma unroll
-        for (int e = 0; e < V; ++e) r.v[e] = v[i].v[V - 1 - e];
-        store_vec<T, V>(out2 + (L - V - p), r);
+            for (int e = 0; e < V; ++e) r.v[e] = v[i].v[V - 1 - e];
+            store_vec<T, V>(out2 + (L - V - p), r);
+        }
 #pragma unroll
         for (int e = 0; e < V; ++e) {
             const int pe = p + e, h = pe / W, w = pe - h * W;
@@ -179,7 +183,7 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
             r.v[V - 1 - e] = v.v[e];
         }
         store_vec<T, V>(out1 + q, v);
-        store_vec<T, V>(out3 + (L - V - q), r);
+        if constexpr (kAll) store_vec<T, V>(out3 + (L - V - q), r);
     }
 }
 
@@ -258,31 +262,47 @@ bool grid_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
            (W + kTile - 1) / kTile <= 65535;
 }
 
+
+template <bool kAll>
+vmb_status launch_scan_planes(const void* x, void* xs, int64_t batch, int64_t channels, int64_t H,
+                              int64_t W, vmb_dtype dt, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>(batch * channels)), block(kPlaneThreads);
+    const int c = int(channels), h = int(H), w = int(W);
+    const int64_t L = H * W;
+    if (dt == VMB_F32) {
+        const float* xi = static_cast<const float*>(x);
+        float* xo = static_cast<float*>(xs);
+        if (L % 4 == 0)
+            hipLaunchKernelGGL((k_cross_scan_plane<float, 4, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+        else
+            hipLaunchKernelGGL((k_cross_scan_plane<float, 1, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+    } else {
+        const bf16_t* xi = static_cast<const bf16_t*>(x);
+        bf16_t* xo = static_cast<bf16_t*>(xs);
+        if (L % 8 == 0)
+            hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 8, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+        else
+            hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 1, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+    }
+    return check_launch();
+}
+
 }  // namespace
+
+bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
+    return plane_fits(batch, channels, H, W);
+}
+
+vmb_status launch_transpose_planes(const void* x, void* xt, int64_t batch, int64_t channels,
+                                   int64_t H, int64_t W, vmb_dtype dt, hipStream_t s) {
+    if (!plane_fits(batch, channels, H, W)) return VMB_ERR_UNSUPPORTED;
+    return launch_scan_planes<false>(x, xt, batch, channels, H, W, dt, s);
+}
 
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
                              int64_t H, int64_t W, vmb_dtype dt, hipStream_t s) {
-    if (plane_fits(batch, channels, H, W)) {
-        const dim3 grid(static_cast<unsigned>(batch * channels)), block(kPlaneThreads);
-        const int c = int(channels), h = int(H), w = int(W);
-        const int64_t L = H * W;
-        if (dt == VMB_F32) {
-            const float* xi = static_cast<const float*>(x);
-            float* xo = static_cast<float*>(xs);
-            if (L % 4 == 0)
-                hipLaunchKernelGGL((k_cross_scan_plane<float, 4>), grid, block, 0, s, xi, xo, c, h, w);
-            else
-                hipLaunchKernelGGL((k_cross_scan_plane<float, 1>), grid, block, 0, s, xi, xo, c, h, w);
-        } else {
-            const bf16_t* xi = static_cast<const bf16_t*>(x);
-            bf16_t* xo = static_cast<bf16_t*>(xs);
-            if (L % 8 == 0)
-                hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 8>), grid, block, 0, s, xi, xo, c, h, w);
-            else
-                hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 1>), grid, block, 0, s, xi, xo, c, h, w);
-        }
-        return check_launch();
-    }
+    if (plane_fits(batch, channels, H, W))
+        return launch_scan_planes<true>(x, xs, batch, channels, H, W, dt, s);
     if (!grid_fits(batch, channels, H, W)) return VMB_ERR_UNSUPPORTED;
     const dim3 grid = tile_grid(batch, channels, H, W), block(kTile, kRows);
     if (dt == VMB_F32)

@@ -77,7 +77,8 @@ template <int N, typename Tin, bool kTwoD>
 __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
-    MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks, int softplus) {
+    const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
+    int softplus) {
     __shared__ float part[kRedWaves][N + 2][kC];
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
@@ -87,7 +88,12 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const int tc = valid ? t : L - 1;  // clamped: every address below stays in bounds
     const size_t bk = static_cast<size_t>(b) * K + k;
     const bool sp = softplus != 0;
-    const int src = kTwoD ? pixel_of(k, tc, H, W) : tc;
+    // 2-D layout: directions 0 / 2 read x at t / L - 1 - t; directions 1 / 3
+    // read the column-major copies xt (when given) at the same positions, or
+    // gather x through the cross-scan map
+    const bool use_xt = kTwoD && xt != nullptr && (k & 1);
+    const int src = !kTwoD ? tc : (use_xt ? (k == 3 ? L - 1 - tc : tc) : pixel_of(k, tc, H, W));
+    const Tin* usrc = use_xt ? xt : u;
     float acc[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) acc[n] = 0.0f;
@@ -100,7 +106,7 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
             const size_t row = (bk * Dc + d) * static_cast<size_t>(L);
             const size_t urow = kTwoD ? (static_cast<size_t>(b) * Dc + d) * L : row;
             dv[j] = to_f32(delta[row + tc]);
-            uv[j] = to_f32(u[urow + src]);
+            uv[j] = to_f32(usrc[urow + src]);
         }
     };
 
@@ -328,7 +334,7 @@ inline int clamp_groups(long long want, int Dc) {
 template <int N, typename Tin, typename Tout, bool kTwoD>
 vmb_status run(const ScanArgs& a) {
     const size_t bkn = static_cast<size_t>(a.batch * a.K);
-    const MeanWsLayout lay = mean_ws_layout(a.batch, a.K, a.L, N, kTwoD);
+    const MeanWsLayout lay = mean_ws_layout(a.batch, a.K, a.channels, a.L, N, kTwoD);
     char* p = static_cast<char*>(a.ws);
     MeanWs ws;
     ws.scan = reinterpret_cast<float*>(p + lay.scan);
@@ -341,9 +347,18 @@ vmb_status run(const ScanArgs& a) {
     const int C = mean_chunk(a.batch, a.K, a.L);
     const int nchunks = (L + C - 1) / C;
     const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
+    // 2-D layout: column-major copies of the planes first, so that every
+    // direction's reduce reads stay coalesced
+    const Tin* xt = nullptr;
+    if (kTwoD && mean_transposes(a.L, true) && cross_plane_fits(a.batch, a.channels, a.H, a.W)) {
+        vmb_status s0 = launch_transpose_planes(a.u, p + lay.xt, a.batch, a.channels, a.H, a.W,
+                                                a.in_dt, a.stream);
+        if (s0 != VMB_OK) return s0;
+        xt = reinterpret_cast<const Tin*>(p + lay.xt);
+    }
     hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD>), grid, dim3(kC * kRedWaves), 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
-                       static_cast<const Tin*>(a.B), a.D, a.dt_bias, ws, K, Dc, L, H, W, C,
+                       static_cast<const Tin*>(a.B), a.D, a.dt_bias, xt, ws, K, Dc, L, H, W, C,
                        nchunks, a.softplus);
     vmb_status st = check_launch();
     if (st != VMB_OK) return st;

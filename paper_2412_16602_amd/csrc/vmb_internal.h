@@ -70,10 +70,15 @@ inline int mean_chunk(int64_t batch, int64_t K, int64_t L) {
 //   agg   [bk][nch][N][2]     : chunk aggregates
 //   carry [bk][nch][N]        : state entering each chunk
 //   ytil  [bk][L]             : 2-D layout only, the reduced output
+//   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL only,
+//                               column-major copies of the input planes
+constexpr int64_t kMeanTransposeMaxL = 6144;  // then H * (W + 1) <= 2 L fits LDS
 struct MeanWsLayout {
-    size_t scan, rmean, agg, carry, ytil, total;
+    size_t scan, rmean, agg, carry, ytil, xt, total;
 };
-inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t L, int64_t N, bool two_d) {
+inline bool mean_transposes(int64_t L, bool two_d) { return two_d && L <= kMeanTransposeMaxL; }
+inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, int64_t L,
+                                   int64_t N, bool two_d) {
     auto up = [](size_t v) { return (v + 255) & ~size_t{255}; };
     const size_t bk = static_cast<size_t>(batch) * static_cast<size_t>(K);
     const int chunk = mean_chunk(batch, K, L);
@@ -84,13 +89,20 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t L, int64_t 
     o.agg = o.rmean + up(bk * L * 4);
     o.carry = o.agg + up(bk * nch * N * 2 * 4);
     o.ytil = o.carry + up(bk * nch * N * 4);
-    o.total = o.ytil + (two_d ? up(bk * L * 4) : 0);
+    o.xt = o.ytil + (two_d ? up(bk * L * 4) : 0);
+    const size_t planes = static_cast<size_t>(batch) * static_cast<size_t>(channels);
+    o.total = o.xt + (mean_transposes(L, two_d) ? up(planes * L * 4) : 0);
     return o;
 }
 
 // Launchers (enqueue only; arguments already validated).
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
                              int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);
+// Column-major copy of every (batch, channel) plane, xt[plane][w * H + h]
+// (direction 1's sequence); only for planes that cross_plane_fits accepts.
+bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W);
+vmb_status launch_transpose_planes(const void* x, void* xt, int64_t batch, int64_t channels,
+                                   int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);
 // Merge with independent input / output element types (fp32 -> bf16 is used
 // by the 2-D scan layouts).
 vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t channels,

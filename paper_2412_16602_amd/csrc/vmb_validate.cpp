@@ -72,7 +72,7 @@ size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t 
         // 2-D layout: per-direction fp32 outputs, folded by the merge pass
         return layout == VMB_LAYOUT_2D ? round_up(static_cast<size_t>(seq) * 4) : 0;
     }
-    return mean_ws_layout(batch, K, L, N, layout == VMB_LAYOUT_2D).total;
+    return mean_ws_layout(batch, K, channels, L, N, layout == VMB_LAYOUT_2D).total;
 }
 
 vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
