@@ -8,21 +8,27 @@
 //   r_mean[t]      = mean_d D[c] u_{d,t}             (skip term, reduced with the scan)
 // then one N-state recurrence per (batch, k) and the broadcast of its output.
 //
-// Three passes over chunks of kMeanChunk (64) positions:
+// Passes over chunks of C <= kMeanChunk (64) positions (C chosen so the chunk
+// count fills the machine, e.g. 49 positions at 4 x 3136):
 //   1. reduce : a workgroup owns one chunk of one (batch, k); lanes own
-//               positions (coalesced loads along t), each of its 8 waves sums
-//               a fixed eighth of the channels (channel parameters are
-//               wave-uniform), and the eighths are added in a fixed order in
-//               LDS. Each state's chunk-local inclusive scan of the pairs
-//               (Abar_mean, B s_mean), composed with
-//               (a1, b1) then (a2, b2) -> (a1 a2, a2 b1 + b2), is stored per
-//               position together with r_mean, and the chunk's aggregate
-//               (its last position) is what the carry pass chains.
-//   2. carry  : one wave per (batch, k, n) scans the chunk aggregates across
-//               lanes (DPP) and stores the state entering each chunk.
+//               positions (coalesced loads along t), each of its 16 waves sums
+//               a fixed sixteenth of the channels (channel parameters are
+//               wave-uniform scalar loads, issued one channel ahead), and the
+//               sixteenths are added in a fixed order in LDS. Each state's
+//               chunk-local inclusive scan of the pairs (Abar_mean, B s_mean),
+//               composed with (a1, b1) then (a2, b2) -> (a1 a2, a2 b1 + b2), is
+//               stored per position together with r_mean; the chunk's
+//               aggregate is its last position's value.
+//   2. carry  : (only with more than 64 chunks) one wave per (batch, k, n)
+//               scans the chunk aggregates across lanes (DPP) and stores the
+//               state entering each chunk; with at most 64 chunks the finish
+//               pass does this scan itself.
 //   3. finish : h[n,t] = P[n,t] * carry[n] + H[n,t], ytilde = sum_n C h + r,
-//               broadcast to every channel (sequence layout) or stored for
-//               the merge-and-broadcast pass (2-D layout).
+//               broadcast to every channel (sequence layout), or stored and
+//               then folded and broadcast by the merge pass (2-D layout).
+// In the 2-D layout directions 1 and 3 read column-major copies of the input
+// planes (made first, one transpose pass) so that every reduce load stays
+// coalesced.
 // All sums run in a fixed order, so results are deterministic.
 #include "vmb_internal.h"
 
@@ -32,7 +38,7 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kC = kMeanChunk;  // positions per chunk = lanes per wave
 constexpr int kRedWaves = 16;   // channel split of the reduce pass
-constexpr int kUnroll = 4;      // channels per load group (two groups in flight)
+constexpr int kUnroll = 4;      // channels per load group
 constexpr int kFinWaves = 4;    // waves of a finish workgroup
 
 // Inclusive scan over the 64 lanes of the (a, b) pairs, in lane order
@@ -110,34 +116,46 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
         }
     };
 
-    // delta / u of the first three channel groups in flight (ring of four)
-    constexpr int kRing = 4;
+    // delta / u of the next channel group in flight (ring of two)
+    constexpr int kRing = 2;
     float dv[kRing][kUnroll], uv[kRing][kUnroll];
 #pragma unroll
     for (int g = 0; g < kRing - 1; ++g)
         if (d0 + g * kUnroll < d1) load_group(d0 + g * kUnroll, dv[g], uv[g]);
-    // Channel parameters are wave-uniform: scalar loads, no staging.
+    // Channel parameters are wave-uniform: scalar loads, issued one channel
+    // ahead so that their latency overlaps the current channel's work.
+    auto load_params = [&](int dch, float (&an)[N], float& bias, float& dskip) {
+        const int c = k * Dc + dch;
+        bias = dt_bias ? dt_bias[c] : 0.0f;
+        dskip = D ? D[c] : 0.0f;
+#pragma unroll
+        for (int n = 0; n < N; ++n) an[n] = A[static_cast<size_t>(c) * N + n];
+    };
+    float an[N], bias = 0.0f, dskip = 0.0f;
+    if (d0 < d1) load_params(d0, an, bias, dskip);
     for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
 #pragma unroll
         for (int g = 0; g < kRing; ++g) {
             const int gd = dd + g * kUnroll;
             if (gd >= d1) break;
-            // keep three groups ahead in flight
+            // keep one group ahead in flight
             const int pf = gd + (kRing - 1) * kUnroll;
             if (pf < d1) load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
 #pragma unroll
             for (int j = 0; j < kUnroll; ++j) {
                 if (gd + j >= d1) break;
-                const int c = k * Dc + gd + j;
-                const float bias = dt_bias ? dt_bias[c] : 0.0f;
-                const float dskip = D ? D[c] : 0.0f;
-                const float* Ac = A + static_cast<size_t>(c) * N;
+                float an_n[N], bias_n, dskip_n;
+                load_params(gd + j + 1 < d1 ? gd + j + 1 : gd + j, an_n, bias_n, dskip_n);
                 const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
                 const float dl2 = dl * kLog2e;
 #pragma unroll
-                for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * Ac[n]);
+                for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * an[n]);
                 s = __builtin_fmaf(dl, uv[g][j], s);
                 r = __builtin_fmaf(dskip, uv[g][j], r);
+#pragma unroll
+                for (int n = 0; n < N; ++n) an[n] = an_n[n];
+                bias = bias_n;
+                dskip = dskip_n;
             }
         }
     }
