@@ -99,12 +99,15 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 
 }  // namespace
 
-bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L >= 512; }
+bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L > kShortMaxL; }
 
 vmb_status launch_full_scan(const ScanArgs& a) {
-    if (use_chunked_full(a)) {
-        if (a.layout == VMB_LAYOUT_SEQ) return launch_full_chunked(a, a.y);
-        vmb_status st = launch_full_chunked(a, a.ws);
+    if (use_chunked_full(a) || use_short_full(a)) {
+        auto run = [&](void* y_seq) {
+            return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq);
+        };
+        if (a.layout == VMB_LAYOUT_SEQ) return run(a.y);
+        vmb_status st = run(a.ws);
         if (st != VMB_OK) return st;
         return launch_cross_merge(a.ws, a.y, a.batch, a.channels, a.H, a.W, VMB_F32, a.out_dt,
                                   a.stream);

@@ -112,6 +112,11 @@ vmb_status launch_full_scan(const ScanArgs& a);
 // Positions-over-lanes full scan (N == 16); writes sequence-layout output to
 // y_seq (a.y for the sequence layout, the fp32 workspace for the 2-D one).
 vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq);
+// Short sequences (L <= kShortMaxL, N == 16): whole sequences in segments of
+// 16 or 32 lanes of one wave; writes sequence-layout output to y_seq.
+constexpr int64_t kShortMaxL = 416;
+bool use_short_full(const ScanArgs& a);
+vmb_status launch_full_short(const ScanArgs& a, void* y_seq);
 // Whether the positions-over-lanes kernel is the better fit for this shape.
 bool use_chunked_full(const ScanArgs& a);
 vmb_status launch_mean_scan(const ScanArgs& a);

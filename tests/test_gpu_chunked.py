@@ -17,7 +17,8 @@ def shape(b, H, W, c, dtype="f32", seed=0):
 
 # L chosen around the run / wave / chunk boundaries (runs of 13 or 16 positions,
 # 64 lanes per wave, 1, 2 or 4 waves per channel)
-LENGTHS = [512, 831, 832, 833, 1663, 1664, 1665, 3136, 3327, 3328, 3329, 4096, 4097, 8193]
+LENGTHS = [417, 500, 512, 831, 832, 833, 1663, 1664, 1665, 3136, 3327, 3328, 3329, 4096, 4097,
+           8193]
 
 
 @pytest.mark.parametrize("L", LENGTHS)
