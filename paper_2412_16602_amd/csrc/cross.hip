@@ -128,13 +128,20 @@ __device__ __forceinline__ void store_vec(T* p, const Vec<T, V>& r) {
 // V elements per lane; L % V == 0 and 16-byte aligned planes when V > 1.
 // kAll = false writes only the column-major copy of each plane (direction 1's
 // sequence), to xs[plane][L].
-template <typename T, int V, bool kAll>
+// TPP threads per plane, kPlaneThreads / TPP planes per workgroup, each with
+// its share of the LDS (small planes are batched, one wave each).
+template <typename T, int V, bool kAll, int TPP>
 __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __restrict__ x,
                                                                     T* __restrict__ xs, int Dc,
-                                                                    int H, int W) {
-    __shared__ T tile[kPlaneLdsWords];
+                                                                    int H, int W, int nplanes) {
+    constexpr int kShare = kPlaneLdsWords / (kPlaneThreads / TPP);
+    __shared__ T tiles[kPlaneLdsWords];
     const int L = H * W, Wp = W + 1;
-    const int plane = blockIdx.x;  // b * Dc + d
+    const int sub = threadIdx.x / TPP, tid = threadIdx.x % TPP;
+    T* tile = tiles + sub * kShare;
+    const int pl = blockIdx.x * (kPlaneThreads / TPP) + sub;  // b * Dc + d
+    const bool active = pl < nplanes;
+    const int plane = active ? pl : nplanes - 1;
     const int b = plane / Dc;
     const int d = plane - b * Dc;
     const T* src = x + static_cast<size_t>(plane) * L;
@@ -146,17 +153,17 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
     const int nv = L / V;
     // every load of this lane issued first (one memory round trip), then
     // directions 0 and 2 from registers and the plane parked (padded) for 1, 3
-    constexpr int kPer = (kPlaneLdsWords / V + kPlaneThreads - 1) / kPlaneThreads;
+    constexpr int kPer = (kShare / V + TPP - 1) / TPP;
     Vec<T, V> v[kPer];
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-        const int j = threadIdx.x + i * kPlaneThreads;
-        if (j < nv) v[i] = load_vec<T, V>(src + j * V);
+        const int j = tid + i * TPP;
+        if (active && j < nv) v[i] = load_vec<T, V>(src + j * V);
     }
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-        const int j = threadIdx.x + i * kPlaneThreads;
-        if (j >= nv) break;
+        const int j = tid + i * TPP;
+        if (!active || j >= nv) break;
         const int p = j * V;
         if constexpr (kAll) {
             store_vec<T, V>(out0 + p, v[i]);
@@ -173,7 +180,7 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
     }
     __syncthreads();
     // directions 1 and 3: position q = w * H + h reads pixel (h, w)
-    for (int j = threadIdx.x; j < nv; j += kPlaneThreads) {
+    for (int j = tid; active && j < nv; j += TPP) {
         const int q = j * V;
         Vec<T, V> v, r;
 #pragma unroll
@@ -187,13 +194,18 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
     }
 }
 
-template <typename Tin, typename Tout, int V>
+template <typename Tin, typename Tout, int V, int TPP>
 __global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* __restrict__ ys,
                                                                      Tout* __restrict__ y, int Dc,
-                                                                     int H, int W) {
-    __shared__ float s13[kPlaneLdsWords];
+                                                                     int H, int W, int nplanes) {
+    constexpr int kShare = kPlaneLdsWords / (kPlaneThreads / TPP);
+    __shared__ float s13s[kPlaneLdsWords];
     const int L = H * W, Wp = W + 1;
-    const int plane = blockIdx.x;
+    const int sub = threadIdx.x / TPP, tid = threadIdx.x % TPP;
+    float* s13 = s13s + sub * kShare;
+    const int pl = blockIdx.x * (kPlaneThreads / TPP) + sub;
+    const bool active = pl < nplanes;
+    const int plane = active ? pl : nplanes - 1;
     const int b = plane / Dc;
     const int d = plane - b * Dc;
     const size_t seq = static_cast<size_t>(L);
@@ -204,12 +216,12 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* 
     Tout* dst = y + static_cast<size_t>(plane) * L;
     const int nv = L / V;
     // every load of this lane issued first (one memory round trip)
-    constexpr int kPer = (kPlaneLdsWords / V + kPlaneThreads - 1) / kPlaneThreads;
+    constexpr int kPer = (kShare / V + TPP - 1) / TPP;
     Vec<Tin, V> a1[kPer], a3[kPer], a0[kPer], a2[kPer];
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-        const int j = threadIdx.x + i * kPlaneThreads;
-        if (j < nv) {
+        const int j = tid + i * TPP;
+        if (active && j < nv) {
             const int o = j * V;
             a1[i] = load_vec<Tin, V>(in1 + o);
             a3[i] = load_vec<Tin, V>(in3 + (L - V - o));
@@ -220,8 +232,8 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* 
     // y1 + y3 of each pixel, in column order (q = w * H + h), parked by pixel
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-        const int j = threadIdx.x + i * kPlaneThreads;
-        if (j >= nv) break;
+        const int j = tid + i * TPP;
+        if (!active || j >= nv) break;
         const int q = j * V;
 #pragma unroll
         for (int e = 0; e < V; ++e) {
@@ -232,8 +244,8 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* 
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-        const int j = threadIdx.x + i * kPlaneThreads;
-        if (j >= nv) break;
+        const int j = tid + i * TPP;
+        if (!active || j >= nv) break;
         const int p = j * V;
         Vec<Tout, V> o;
 #pragma unroll
@@ -263,26 +275,45 @@ bool grid_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
 }
 
 
+// Threads per plane: one wave for planes of up to 1024 padded words (12 per
+// workgroup), else the whole block (larger planes gain from the extra loads
+// in flight per plane more than from batching).
+inline int plane_tpp(int64_t H, int64_t W) {
+    return H * (W + 1) <= kPlaneLdsWords / 12 ? 64 : kPlaneThreads;
+}
+
+template <typename T, int V, bool kAll>
+void launch_scan_tpp(const T* xi, T* xo, int64_t planes, int c, int h, int w, hipStream_t s) {
+    const int tpp = plane_tpp(h, w);
+    const int ppw = kPlaneThreads / tpp;
+    const dim3 grid(static_cast<unsigned>((planes + ppw - 1) / ppw)), block(kPlaneThreads);
+    const int np = static_cast<int>(planes);
+    if (tpp == 64)
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 64>), grid, block, 0, s, xi, xo, c, h, w, np);
+    else
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, kPlaneThreads>), grid, block, 0, s, xi, xo,
+                           c, h, w, np);
+}
+
 template <bool kAll>
 vmb_status launch_scan_planes(const void* x, void* xs, int64_t batch, int64_t channels, int64_t H,
                               int64_t W, vmb_dtype dt, hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>(batch * channels)), block(kPlaneThreads);
     const int c = int(channels), h = int(H), w = int(W);
-    const int64_t L = H * W;
+    const int64_t L = H * W, planes = batch * channels;
     if (dt == VMB_F32) {
         const float* xi = static_cast<const float*>(x);
         float* xo = static_cast<float*>(xs);
         if (L % 4 == 0)
-            hipLaunchKernelGGL((k_cross_scan_plane<float, 4, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+            launch_scan_tpp<float, 4, kAll>(xi, xo, planes, c, h, w, s);
         else
-            hipLaunchKernelGGL((k_cross_scan_plane<float, 1, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+            launch_scan_tpp<float, 1, kAll>(xi, xo, planes, c, h, w, s);
     } else {
         const bf16_t* xi = static_cast<const bf16_t*>(x);
         bf16_t* xo = static_cast<bf16_t*>(xs);
         if (L % 8 == 0)
-            hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 8, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+            launch_scan_tpp<bf16_t, 8, kAll>(xi, xo, planes, c, h, w, s);
         else
-            hipLaunchKernelGGL((k_cross_scan_plane<bf16_t, 1, kAll>), grid, block, 0, s, xi, xo, c, h, w);
+            launch_scan_tpp<bf16_t, 1, kAll>(xi, xo, planes, c, h, w, s);
     }
     return check_launch();
 }
@@ -315,19 +346,31 @@ vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t cha
     return check_launch();
 }
 
+template <typename Tin, typename Tout, int V>
+void launch_merge_tpp(const Tin* in, Tout* out, int64_t planes, int c, int h, int w, hipStream_t s) {
+    const int tpp = plane_tpp(h, w);
+    const int ppw = kPlaneThreads / tpp;
+    const dim3 grid(static_cast<unsigned>((planes + ppw - 1) / ppw)), block(kPlaneThreads);
+    const int np = static_cast<int>(planes);
+    if (tpp == 64)
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, 64>), grid, block, 0, s, in, out, c, h, w, np);
+    else
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, kPlaneThreads>), grid, block, 0, s, in, out,
+                           c, h, w, np);
+}
+
 template <typename Tin, typename Tout>
 void launch_merge_plane(const void* ys, void* y, int64_t batch, int64_t channels, int64_t H,
                         int64_t W, hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>(batch * channels)), block(kPlaneThreads);
     const int c = int(channels), h = int(H), w = int(W);
     const Tin* in = static_cast<const Tin*>(ys);
     Tout* out = static_cast<Tout*>(y);
     // 16-byte vectors on both sides: 4 elements of the wider type
     constexpr int V = (sizeof(Tin) == 2 && sizeof(Tout) == 2) ? 8 : 4;
     if ((H * W) % V == 0)
-        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V>), grid, block, 0, s, in, out, c, h, w);
+        launch_merge_tpp<Tin, Tout, V>(in, out, batch * channels, c, h, w, s);
     else
-        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, 1>), grid, block, 0, s, in, out, c, h, w);
+        launch_merge_tpp<Tin, Tout, 1>(in, out, batch * channels, c, h, w, s);
 }
 
 vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t channels,
