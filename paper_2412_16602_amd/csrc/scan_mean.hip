@@ -38,7 +38,9 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kC = kMeanChunk;  // positions per chunk = lanes per wave
 constexpr int kRedWaves = 16;   // channel split of the reduce pass
-constexpr int kUnroll = 4;      // channels per load group
+constexpr int kAhead = 4;       // channels of delta / u in flight per wave
+
+__device__ float g_zero = 0.0f;  // stands in for an absent dt_bias / D (never written)
 constexpr int kFinWaves = 4;    // waves of a finish workgroup
 
 // Inclusive scan over the 64 lanes of the (a, b) pairs, in lane order
@@ -69,7 +71,7 @@ __device__ __forceinline__ void wave_scan(float& a, float& b) {
 // Workspace layout, per (batch, k) = bk, for L positions and nch chunks:
 //   scan[bk][n][t][2] : chunk-local inclusive (P, H) of state n at position t
 //   rmean[bk][t]      : r_mean
-//   agg[bk][c][n][2]  : chunk aggregates (copy of the last position's scan)
+//   agg[bk][n][c][2]  : chunk aggregates (copy of the last position's scan)
 //   carry[bk][c][n]   : state entering chunk c
 struct MeanWs {
     float* scan;
@@ -85,7 +87,13 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
     int softplus) {
-    __shared__ float part[kRedWaves][N + 2][kC];
+    // Each wave's slice part[wv] first holds its channel parameters (two
+    // buffers of kAhead rows: A[c, 0..N) log2(e), dt_bias[c], D[c]), read back as
+    // wave-uniform broadcasts, and afterwards its partial sums.
+    constexpr int kPS = (N + 2 + 3) & ~3;  // parameter row stride (16-byte rows)
+    static_assert(2 * kAhead * kPS <= (N + 2) * kC, "parameter buffers fit a wave's slice");
+    static_assert(kAhead <= 32, "parameter row layout");
+    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
@@ -100,62 +108,114 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const bool use_xt = kTwoD && xt != nullptr && (k & 1);
     const int src = !kTwoD ? tc : (use_xt ? (k == 3 ? L - 1 - tc : tc) : pixel_of(k, tc, H, W));
     const Tin* usrc = use_xt ? xt : u;
+    // byte offsets of this lane within a row (32-bit, non-negative)
+    const unsigned toff = static_cast<unsigned>(tc) * sizeof(Tin);
+    const unsigned soff = static_cast<unsigned>(src) * sizeof(Tin);
     float acc[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) acc[n] = 0.0f;
     float s = 0.0f, r = 0.0f;
     const int d0 = (wv * Dc) / kRedWaves, d1 = ((wv + 1) * Dc) / kRedWaves;
-    auto load_group = [&](int dd, float (&dv)[kUnroll], float (&uv)[kUnroll]) {
+    const int nw = d1 - d0;  // channels of this wave
+    float* prm = &part[wv][0][0];
+    const size_t cw = static_cast<size_t>(k) * Dc + d0;  // parameter row of the wave's first channel
+    // absent dt_bias / D read as zeros (a select, not a branch)
+    const float* pbias = dt_bias ? dt_bias : &g_zero;
+    const float* pskip = D ? D : &g_zero;
+    const int bias_stride = dt_bias ? 1 : 0, skip_stride = D ? 1 : 0;
+
+    // delta / u of wave channel i (clamped to the wave's last channel)
+    auto load_ch = [&](int i, float& dv, float& uv) {
+        // wave-uniform row bases (scalar registers), one lane offset each
+        const int d = d0 + (i < nw ? i : nw - 1);
+        const size_t row = (bk * Dc + d) * static_cast<size_t>(L);
+        const size_t urow = kTwoD ? (static_cast<size_t>(b) * Dc + d) * L : row;
+        const char* dp = reinterpret_cast<const char*>(delta + row);
+        const char* up = reinterpret_cast<const char*>(usrc + urow);
+        dv = to_f32(*reinterpret_cast<const Tin*>(dp + toff));
+        uv = to_f32(*reinterpret_cast<const Tin*>(up + soff));
+    };
+    // parameters of wave channels i0 .. i0 + kAhead - 1 (clamped): global
+    // loads into registers, later written to LDS buffer buf
+    constexpr int kPA = (kAhead * N + kC - 1) / kC;
+    auto load_par = [&](int i0, float (&pa)[kPA], float& pbd) {
 #pragma unroll
-        for (int j = 0; j < kUnroll; ++j) {
-            const int d = dd + j < d1 ? dd + j : d1 - 1;
-            const size_t row = (bk * Dc + d) * static_cast<size_t>(L);
-            const size_t urow = kTwoD ? (static_cast<size_t>(b) * Dc + d) * L : row;
-            dv[j] = to_f32(delta[row + tc]);
-            uv[j] = to_f32(usrc[urow + src]);
+        for (int m = 0; m < kPA; ++m) {
+            const int idx = (lane + m * kC) % (kAhead * N);
+            const int i = i0 + idx / N;
+            pa[m] = A[(cw + (i < nw ? i : nw - 1)) * N + idx % N];
         }
+        const int i = i0 + (lane % kAhead);
+        const size_t c = cw + (i < nw ? i : nw - 1);
+        pbd = lane < 32 ? pbias[c * bias_stride] : pskip[c * skip_stride];
+    };
+    auto write_par = [&](int buf, const float (&pa)[kPA], float pbd) {
+        float* base = prm + buf * kAhead * kPS;
+#pragma unroll
+        for (int m = 0; m < kPA; ++m) {
+            const int idx = lane + m * kC;
+            if (idx < kAhead * N) base[(idx / N) * kPS + idx % N] = pa[m] * kLog2e;
+        }
+        if (lane < kAhead) base[lane * kPS + N] = pbd;
+        else if (lane >= 32 && lane < 32 + kAhead) base[(lane - 32) * kPS + N + 1] = pbd;
+    };
+    auto read_par = [&](int buf, int i, float (&an)[N], float& bias, float& dskip) {
+        const float* row = prm + buf * kAhead * kPS + i * kPS;
+#pragma unroll
+        for (int n = 0; n < N; ++n) an[n] = row[n];
+        bias = row[N];
+        dskip = row[N + 1];
+    };
+    auto channel = [&](const float (&an)[N], float bias, float dskip, float dv, float uv) {
+        const float dl = valid ? timescale(dv + bias, sp) : 0.0f;
+#pragma unroll
+        for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl * an[n]);  // an = A log2(e)
+        s = __builtin_fmaf(dl, uv, s);
+        r = __builtin_fmaf(dskip, uv, r);
+        // the sums are formed here, not sunk towards their next use (which
+        // would keep every channel's parameters live)
+#pragma unroll
+        for (int n = 0; n < N; ++n) asm volatile("" : "+v"(acc[n]));
+        asm volatile("" : "+v"(s), "+v"(r));
     };
 
-    // delta / u of the next channel group in flight (ring of two)
-    constexpr int kRing = 2;
-    float dv[kRing][kUnroll], uv[kRing][kUnroll];
+    if (nw > 0) {
+        // parameters of the first block, then delta / u of its kAhead
+        // channels: a ring refilled kAhead channels ahead of use
+        float pa[kPA], pbd;
+        load_par(0, pa, pbd);
+        // issued before the ring's loads, so that writing them out waits for
+        // them alone
+        __builtin_amdgcn_sched_barrier(0);
+        float dv[kAhead], uv[kAhead];
 #pragma unroll
-    for (int g = 0; g < kRing - 1; ++g)
-        if (d0 + g * kUnroll < d1) load_group(d0 + g * kUnroll, dv[g], uv[g]);
-    // Channel parameters are wave-uniform: scalar loads, issued one channel
-    // ahead so that their latency overlaps the current channel's work.
-    auto load_params = [&](int dch, float (&an)[N], float& bias, float& dskip) {
-        const int c = k * Dc + dch;
-        bias = dt_bias ? dt_bias[c] : 0.0f;
-        dskip = D ? D[c] : 0.0f;
+        for (int j = 0; j < kAhead; ++j) load_ch(j, dv[j], uv[j]);
+        write_par(0, pa, pbd);
+        const int nb = nw / kAhead;  // full blocks; the rest is the tail
+        for (int blk = 0; blk < nb; ++blk) {
+            const int buf = blk & 1, i0 = blk * kAhead;
+            load_par(i0 + kAhead, pa, pbd);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int n = 0; n < N; ++n) an[n] = A[static_cast<size_t>(c) * N + n];
-    };
-    float an[N], bias = 0.0f, dskip = 0.0f;
-    if (d0 < d1) load_params(d0, an, bias, dskip);
-    for (int dd = d0; dd < d1; dd += kRing * kUnroll) {
+            for (int j = 0; j < kAhead; ++j) {
+                // one channel at a time (no hoisting across channels, which
+                // would cost registers the load ring needs)
+                __builtin_amdgcn_sched_barrier(0);
+                float an[N], bias, dskip;
+                read_par(buf, j, an, bias, dskip);
+                channel(an, bias, dskip, dv[j], uv[j]);
+                load_ch(i0 + kAhead + j, dv[j], uv[j]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            write_par(buf ^ 1, pa, pbd);
+        }
+        const int rem = nw - nb * kAhead;
 #pragma unroll
-        for (int g = 0; g < kRing; ++g) {
-            const int gd = dd + g * kUnroll;
-            if (gd >= d1) break;
-            // keep one group ahead in flight
-            const int pf = gd + (kRing - 1) * kUnroll;
-            if (pf < d1) load_group(pf, dv[(g + kRing - 1) % kRing], uv[(g + kRing - 1) % kRing]);
-#pragma unroll
-            for (int j = 0; j < kUnroll; ++j) {
-                if (gd + j >= d1) break;
-                float an_n[N], bias_n, dskip_n;
-                load_params(gd + j + 1 < d1 ? gd + j + 1 : gd + j, an_n, bias_n, dskip_n);
-                const float dl = valid ? timescale(dv[g][j] + bias, sp) : 0.0f;
-                const float dl2 = dl * kLog2e;
-#pragma unroll
-                for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl2 * an[n]);
-                s = __builtin_fmaf(dl, uv[g][j], s);
-                r = __builtin_fmaf(dskip, uv[g][j], r);
-#pragma unroll
-                for (int n = 0; n < N; ++n) an[n] = an_n[n];
-                bias = bias_n;
-                dskip = dskip_n;
+        for (int j = 0; j < kAhead - 1; ++j) {
+            if (j < rem) {
+                float an[N], bias, dskip;
+                read_par(nb & 1, j, an, bias, dskip);
+                channel(an, bias, dskip, dv[j], uv[j]);
             }
         }
     }
@@ -177,7 +237,7 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
         if (valid) ws.rmean[bk * L + t] = rm * inv;
     }
     float* scan_bk = ws.scan + bk * N * L * 2;
-    float* agg_c = ws.agg + (bk * nchunks + chunk) * N * 2;
+    float* agg_bk = ws.agg + bk * N * nchunks * 2;
     for (int n = wv; n < N; n += kRedWaves) {
         float am = 0.0f;
         for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
@@ -190,10 +250,9 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
             float2 v = make_float2(a, bb);
             *reinterpret_cast<float2*>(scan_bk + (static_cast<size_t>(n) * L + t) * 2) = v;
         }
-        if (lane == kC - 1) {
-            agg_c[2 * n] = a;
-            agg_c[2 * n + 1] = bb;
-        }
+        if (lane == kC - 1)
+            *reinterpret_cast<float2*>(agg_bk + (static_cast<size_t>(n) * nchunks + chunk) * 2) =
+                make_float2(a, bb);
     }
 }
 
@@ -207,9 +266,10 @@ __global__ __launch_bounds__(kWave) void k_mean_carry(MeanWs ws, int N, int nchu
         const int c = c0 + lane;
         float a = 1.0f, bb = 0.0f;
         if (c < nchunks) {
-            const size_t o = ((bk * nchunks + c) * N + n) * 2;
-            a = ws.agg[o];
-            bb = ws.agg[o + 1];
+            const float2 g = *reinterpret_cast<const float2*>(
+                ws.agg + ((bk * N + n) * nchunks + c) * 2);
+            a = g.x;
+            bb = g.y;
         }
         wave_scan(a, bb);
         // state entering chunk c = carry composed with the chunks before c
@@ -248,9 +308,10 @@ __device__ __forceinline__ void ch_partials(const MeanWs& ws, const Tin* __restr
             gb[i][j] = 0.0f;
             if (inline_carry) {
                 if (on && lane < nchunks) {
-                    const size_t o = ((bk[i] * nchunks + lane) * N + nn) * 2;
-                    ga[i][j] = ws.agg[o];
-                    gb[i][j] = ws.agg[o + 1];
+                    const float2 g = *reinterpret_cast<const float2*>(
+                        ws.agg + ((bk[i] * N + nn) * nchunks + lane) * 2);
+                    ga[i][j] = g.x;
+                    gb[i][j] = g.y;
                 }
             } else {
                 gb[i][j] = ws.carry[(bk[i] * nchunks + ch) * N + nn];
