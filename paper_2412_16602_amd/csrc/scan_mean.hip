@@ -8,13 +8,13 @@
 //   r_mean[t]      = mean_d D[c] u_{d,t}             (skip term, reduced with the scan)
 // then one N-state recurrence per (batch, k) and the broadcast of its output.
 //
-// Passes over chunks of C <= kMeanChunk (64) positions (C chosen so the chunk
-// count fills the machine, e.g. 49 positions at 4 x 3136):
+// Passes over chunks of C = 64 positions:
 //   1. reduce : a workgroup owns one chunk of one (batch, k); lanes own
 //               positions (coalesced loads along t), each of its 16 waves sums
-//               a fixed sixteenth of the channels (channel parameters are
-//               wave-uniform scalar loads, issued one channel ahead), and the
-//               sixteenths are added in a fixed order in LDS. Each state's
+//               a fixed sixteenth of the channels (their parameters staged in
+//               the wave's LDS slice and read as broadcasts; delta / u of the
+//               next channels in flight), and the sixteenths are added in a
+//               fixed order in LDS. Each state's
 //               chunk-local inclusive scan of the pairs (Abar_mean, B s_mean),
 //               composed with (a1, b1) then (a2, b2) -> (a1 a2, a2 b1 + b2), is
 //               stored per position together with r_mean; the chunk's

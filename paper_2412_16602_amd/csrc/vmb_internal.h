@@ -42,26 +42,11 @@ size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t 
 // Chunk length (positions) of the mean variant's reduce / carry / finish passes.
 constexpr int kMeanChunk = 64;
 
-// Positions per chunk of the mean variant (at most kMeanChunk): the number of
-// chunks over all (batch, direction) sequences is rounded towards a multiple
-// of 256 workgroups (the compute units of one MI355X) where that wastes few
-// lanes, e.g. 49 positions (256 workgroups) for 4 x 3136.
-inline int mean_chunk(int64_t batch, int64_t K, int64_t L) {
-    const int64_t seqs = batch * K;
-    int best = kMeanChunk;
-    double best_cost = 1e300;
-    for (int c = 32; c <= kMeanChunk; ++c) {
-        const int64_t wgs = seqs * ((L + c - 1) / c);
-        const int64_t rounds = (wgs + 255) / 256;
-        // ~ time per CU: rounds of workgroups, each a fixed overhead plus c positions
-        const double cost = static_cast<double>(rounds) * (c + 16);
-        if (cost < best_cost - 1e-9) {
-            best_cost = cost;
-            best = c;
-        }
-    }
-    return best;
-}
+// Positions per chunk of the mean variant. Lanes are positions, so a
+// workgroup's time does not depend on the chunk length; full 64-position
+// chunks keep every row segment the reduce reads whole (fewer, aligned cache
+// lines) at no cost in parallelism: the per-SIMD channel work is the same.
+inline int mean_chunk(int64_t /*batch*/, int64_t /*K*/, int64_t /*L*/) { return kMeanChunk; }
 
 // Byte offsets of the mean variant's workspace regions (each 256-byte
 // aligned), for bk = batch * K direction sequences of L positions:
