@@ -30,6 +30,10 @@
 // planes (made first, one transpose pass) so that every reduce load stays
 // coalesced.
 // All sums run in a fixed order, so results are deterministic.
+#include <atomic>
+#include <chrono>
+#include <random>
+
 #include "vmb_internal.h"
 
 namespace vmb {
@@ -81,19 +85,20 @@ struct MeanWs {
     float* ytil;  // 2-D layout: reduced output ytilde[bk][t]
 };
 
+// Reduce stage of one chunk (chunk blockIdx.x of sequence (blockIdx.z,
+// blockIdx.y)): every wave's partial sums over its channels, for the lanes'
+// positions, left in part[wv][0..N+2) (exp sums per state, s, r).
 template <int N, typename Tin, bool kTwoD>
-__global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
-    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
-    const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
-    const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
-    int softplus) {
+__device__ __forceinline__ void reduce_partials(
+    float (*part)[N + 2][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
+    const float* __restrict__ A, const float* __restrict__ D, const float* __restrict__ dt_bias,
+    const Tin* __restrict__ xt, int K, int Dc, int L, int H, int W, int C, int softplus) {
     // Each wave's slice part[wv] first holds its channel parameters (two
     // buffers of kAhead rows: A[c, 0..N) log2(e), dt_bias[c], D[c]), read back as
     // wave-uniform broadcasts, and afterwards its partial sums.
     constexpr int kPS = (N + 2 + 3) & ~3;  // parameter row stride (16-byte rows)
     static_assert(2 * kAhead * kPS <= (N + 2) * kC, "parameter buffers fit a wave's slice");
     static_assert(kAhead <= 32, "parameter row layout");
-    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
@@ -223,7 +228,24 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     for (int n = 0; n < N; ++n) part[wv][n][lane] = acc[n];
     part[wv][N][lane] = s;
     part[wv][N + 1][lane] = r;
+}
+
+template <int N, typename Tin, bool kTwoD>
+__global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
+    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
+    const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
+    const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
+    int softplus) {
+    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
+    reduce_partials<N, Tin, kTwoD>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C, softplus);
     __syncthreads();
+    const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x % kC;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
+    const int t = chunk * C + lane;
+    const bool valid = lane < C && t < L;
+    const int tc = valid ? t : L - 1;
+    const size_t bk = static_cast<size_t>(b) * K + k;
 
     // channel groups added in a fixed order; wave w then scans states
     // w, w + 16, ... of this chunk
@@ -278,6 +300,128 @@ __global__ __launch_bounds__(kWave) void k_mean_carry(MeanWs ws, int N, int nchu
         if (c < nchunks) ws.carry[(bk * nchunks + c) * N + n] = cin;
         const float la = __shfl(a, kWave - 1, kWave), lb = __shfl(bb, kWave - 1, kWave);
         carry = __builtin_fmaf(la, carry, lb);
+    }
+}
+
+// All three passes in one launch, for sequences of at most 64 chunks. After
+// its reduce, each workgroup publishes its chunk aggregates and, once those
+// stores are performed, raises its flag (the call's epoch: a 64-bit value
+// never reused, so flags left by earlier calls, or never written, do not
+// match); it then waits for the
+// flags of the earlier chunks of its sequence, scans their aggregates into
+// the state entering its own chunk, and forms and stores its outputs.
+// Workgroups wait only on lower-numbered workgroups of their own sequence
+// (chunk is the fastest grid dimension), which are dispatched no later, so
+// the lowest unfinished workgroup never waits; every wait is also bounded
+// by a spin limit, so the kernel ends whatever happens.
+constexpr int kSpinLimit = 1 << 16;
+constexpr long long kFusedMaxGrid = 2048;
+
+// (a, b) pairs exchanged between workgroups: 64-bit device-scope atomic
+// accesses, coherent across the chip's L2 caches without cache-wide
+// write-back or invalidation.
+__device__ __forceinline__ void put_pair(float* p, float a, float b) {
+    const unsigned long long v = (static_cast<unsigned long long>(__float_as_uint(b)) << 32) |
+                                 __float_as_uint(a);
+    __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void get_pair(float* p, float& a, float& b) {
+    const unsigned long long v = __hip_atomic_load(reinterpret_cast<unsigned long long*>(p),
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a = __uint_as_float(static_cast<unsigned>(v));
+    b = __uint_as_float(static_cast<unsigned>(v >> 32));
+}
+
+template <int N, typename Tin, typename Tout, bool kTwoD>
+__global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
+    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
+    const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
+    const float* __restrict__ dt_bias, const Tin* __restrict__ xt, MeanWs ws,
+    unsigned long long* __restrict__ flags, unsigned long long epoch, Tout* __restrict__ y, int K,
+    int Dc, int L, int H, int W, int nchunks, int softplus) {
+    static_assert(N <= kRedWaves, "one state per wave");
+    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
+    __shared__ float yst[kRedWaves][kC];  // C h of state n at each position
+    __shared__ float rsh[kC];             // r_mean at each position
+    reduce_partials<N, Tin, kTwoD>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, kC,
+                                   softplus);
+    __syncthreads();
+    const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x % kC;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
+    const int t = chunk * kC + lane;
+    const bool valid = t < L;
+    const int tc = valid ? t : L - 1;
+    const size_t bk = static_cast<size_t>(b) * K + k;
+    const float inv = 1.0f / static_cast<float>(Dc);
+    float* agg_bk = ws.agg + bk * N * nchunks * 2;
+
+    // channel groups added in a fixed order; wave n scans state n
+    float a = 1.0f, bb = 0.0f, cv = 0.0f;
+    if (wv < N) {
+        const int n = wv;
+        cv = valid ? to_f32(Cm[(bk * N + n) * L + tc]) : 0.0f;
+        float sm = 0.0f, am = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) sm += part[w][N][lane];
+        for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
+        sm *= inv;
+        am *= inv;
+        // positions past the end act as the identity (1, 0)
+        a = valid ? am : 1.0f;
+        bb = valid ? to_f32(Bm[(bk * N + n) * L + tc]) * sm : 0.0f;
+        wave_scan(a, bb);
+        if (lane == kC - 1) put_pair(agg_bk + (static_cast<size_t>(n) * nchunks + chunk) * 2, a, bb);
+    } else if (wv == N) {
+        float rm = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) rm += part[w][N + 1][lane];
+        rsh[lane] = rm * inv;
+    }
+    if (N == kRedWaves && wv == 0) {  // no spare wave: wave 0 sums r_mean too
+        float rm = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) rm += part[w][N + 1][lane];
+        rsh[lane] = rm * inv;
+    }
+    // publish: the aggregates (device-coherent stores) are performed before
+    // the flag is stored
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_store(flags + bk * nchunks + chunk, epoch, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    // wait for the earlier chunks (lanes = chunks) of this sequence
+    if (wv == 0 && chunk > 0) {
+        bool ready = lane >= chunk;
+        for (int spin = 0; spin < kSpinLimit; ++spin) {
+            if (!ready)
+                ready = __hip_atomic_load(flags + bk * nchunks + lane, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT) == epoch;
+            if (__all(ready)) break;
+            __builtin_amdgcn_s_sleep(2);
+        }
+    }
+    __syncthreads();
+    if (wv < N) {
+        const int n = wv;
+        // state entering this chunk: scan of the earlier chunks' aggregates
+        // (device-coherent loads, issued after the flags were seen)
+        float ga = 1.0f, gb = 0.0f;
+        if (lane < chunk) get_pair(agg_bk + (static_cast<size_t>(n) * nchunks + lane) * 2, ga, gb);
+        wave_scan(ga, gb);
+        const float prev = __shfl(gb, chunk > 0 ? chunk - 1 : 0, kWave);
+        const float cin = chunk > 0 ? prev : 0.0f;
+        yst[n][lane] = cv * __builtin_fmaf(a, cin, bb);
+    }
+    __syncthreads();
+    if (!valid) return;
+    float yt = rsh[lane];
+#pragma unroll
+    for (int n = 0; n < N; ++n) yt += yst[n][lane];
+    if constexpr (kTwoD) {
+        if (wv == 0) ws.ytil[bk * L + t] = yt;
+    } else {
+        const Tout o = from_f32<Tout>(yt);
+        for (int d = wv; d < Dc; d += kRedWaves) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
     }
 }
 
@@ -410,6 +554,34 @@ inline int clamp_groups(long long want, int Dc) {
     return static_cast<int>(want < 1 ? 1 : (want > most ? most : want));
 }
 
+template <typename Tout>
+vmb_status launch_merge_broadcast(const float* ytil, const ScanArgs& a) {
+    const int Dc = int(a.channels), H = int(a.H), W = int(a.W), L = H * W;
+    const int pblk = (L + 255) / 256;
+    const long long mwant = (512 + pblk * a.batch - 1) / (pblk * a.batch);
+    const int mgroups = clamp_groups(mwant, Dc);
+    hipLaunchKernelGGL(k_mean_merge_broadcast<Tout>,
+                       dim3(pblk, static_cast<unsigned>(mgroups), unsigned(a.batch)), dim3(256), 0,
+                       a.stream, ytil, static_cast<Tout*>(a.y), Dc, H, W, mgroups);
+    return check_launch();
+}
+
+// Flag value of one call of the fused pass: a process-wide counter started
+// at a random 64-bit value (never 0), so that no flag left in a workspace by
+// an earlier call, or by whatever the memory held before, can match it.
+unsigned long long next_epoch() {
+    static std::atomic<unsigned long long> counter{[] {
+        std::random_device rd;
+        const unsigned long long seed =
+            (static_cast<unsigned long long>(rd()) << 32) ^ rd() ^
+            static_cast<unsigned long long>(
+                std::chrono::steady_clock::now().time_since_epoch().count());
+        return seed | 1ull;
+    }()};
+    unsigned long long e = counter.fetch_add(2, std::memory_order_relaxed);
+    return e ? e : counter.fetch_add(2, std::memory_order_relaxed);
+}
+
 template <int N, typename Tin, typename Tout, bool kTwoD>
 vmb_status run(const ScanArgs& a) {
     const size_t bkn = static_cast<size_t>(a.batch * a.K);
@@ -425,6 +597,12 @@ vmb_status run(const ScanArgs& a) {
     const int K = int(a.K), Dc = int(a.channels), L = int(a.L), H = int(a.H), W = int(a.W);
     const int C = mean_chunk(a.batch, a.K, a.L);
     const int nchunks = (L + C - 1) / C;
+    // One launch for all passes when every sequence has at most 64 chunks and
+    // the grid is small (up to 8 workgroups per compute unit): with many more
+    // rounds of workgroups, time spent waiting for an earlier chunk would
+    // hold a compute unit that the separate passes keep busy.
+    const long long wgs = static_cast<long long>(nchunks) * a.K * a.batch;
+    const bool fused = C == kC && nchunks <= kWave && (nchunks == 1 || wgs <= kFusedMaxGrid);
     const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
     // 2-D layout: column-major copies of the planes first, so that every
     // direction's reduce reads stay coalesced
@@ -434,6 +612,17 @@ vmb_status run(const ScanArgs& a) {
                                                 a.in_dt, a.stream);
         if (s0 != VMB_OK) return s0;
         xt = reinterpret_cast<const Tin*>(p + lay.xt);
+    }
+    if (fused) {
+        hipLaunchKernelGGL((k_mean_fused<N, Tin, Tout, kTwoD>), grid, dim3(kC * kRedWaves), 0,
+                           a.stream, static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta),
+                           a.A, static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D,
+                           a.dt_bias, xt, ws, reinterpret_cast<unsigned long long*>(p + lay.flags),
+                           next_epoch(), static_cast<Tout*>(a.y), K, Dc, L, H, W, nchunks,
+                           a.softplus);
+        const vmb_status sf = check_launch();
+        if (sf != VMB_OK || !kTwoD) return sf;
+        return launch_merge_broadcast<Tout>(ws.ytil, a);
     }
     hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD>), grid, dim3(kC * kRedWaves), 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
@@ -462,13 +651,7 @@ vmb_status run(const ScanArgs& a) {
                        static_cast<Tout*>(a.y), K, Dc, L, C, nchunks, groups, inline_carry);
     st = check_launch();
     if (st != VMB_OK || !kTwoD) return st;
-    const int pblk = (L + 255) / 256;
-    const long long mwant = (512 + pblk * a.batch - 1) / (pblk * a.batch);
-    const int mgroups = clamp_groups(mwant, Dc);
-    hipLaunchKernelGGL(k_mean_merge_broadcast<Tout>,
-                       dim3(pblk, static_cast<unsigned>(mgroups), unsigned(a.batch)), dim3(256), 0,
-                       a.stream, ws.ytil, static_cast<Tout*>(a.y), Dc, H, W, mgroups);
-    return check_launch();
+    return launch_merge_broadcast<Tout>(ws.ytil, a);
 }
 
 template <int N, typename Tin, typename Tout>

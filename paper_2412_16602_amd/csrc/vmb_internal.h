@@ -59,7 +59,7 @@ inline int mean_chunk(int64_t /*batch*/, int64_t /*K*/, int64_t /*L*/) { return 
 //                               column-major copies of the input planes
 constexpr int64_t kMeanTransposeMaxL = 6144;  // then H * (W + 1) <= 2 L fits LDS
 struct MeanWsLayout {
-    size_t scan, rmean, agg, carry, ytil, xt, total;
+    size_t scan, rmean, agg, carry, ytil, xt, flags, total;
 };
 inline bool mean_transposes(int64_t L, bool two_d) { return two_d && L <= kMeanTransposeMaxL; }
 inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, int64_t L,
@@ -76,7 +76,8 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, i
     o.ytil = o.carry + up(bk * nch * N * 4);
     o.xt = o.ytil + (two_d ? up(bk * L * 4) : 0);
     const size_t planes = static_cast<size_t>(batch) * static_cast<size_t>(channels);
-    o.total = o.xt + (mean_transposes(L, two_d) ? up(planes * L * 4) : 0);
+    o.flags = o.xt + (mean_transposes(L, two_d) ? up(planes * L * 4) : 0);
+    o.total = o.flags + up(bk * nch * 8);  // one 64-bit flag per chunk
     return o;
 }
 
