@@ -132,6 +132,20 @@ def gpu_bench(args):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / steps  # us per call
 
+    def per_call(call, n):
+        """Each call bracketed by its own events: p10 / median / p90 in us."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n)]
+        for i, (a, b) in enumerate(ev):
+            a.record(stream)
+            call(i)
+            b.record(stream)
+        torch.cuda.synchronize()
+        t = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+        return {"p10": round(float(np.percentile(t, 10)), 3),
+                "p50": round(float(np.percentile(t, 50)), 3),
+                "p90": round(float(np.percentile(t, 90)), 3)}
+
     res = {}
     # --- the step: SS2D forward, 2-D layout, full and mean
     for variant in ("full", "mean"):
@@ -142,7 +156,8 @@ def gpu_bench(args):
         us = timed(call, args.steps, args.warmup)
         wall = time.perf_counter() - t0
         warm = timed(runner(variant, sets[:1], lay), args.steps, 2)
-        res[f"ss2d_{variant}"] = dict(us=us, warm_us=warm, wall_s=wall)
+        dist = per_call(call, min(args.steps, 100))
+        res[f"ss2d_{variant}"] = dict(us=us, warm_us=warm, wall_s=wall, dist=dist)
         del sets
     # --- dominant kernel alone: the scan, sequence layout (one kernel per call for full)
     for variant in ("full", "mean"):
@@ -215,7 +230,18 @@ def cpu_baseline(budget_s: float):
             break
     return dict(value=t_total / reps * 1e6, unit="us/call", cores=threads, kind="oracle",
                 sample=f"{reps} x one SS2D forward (cross-scan, full scan, merge) at 1x56x56, "
-                       f"192 channels, N=16, fp64")
+                       f"192 channels, N=16, fp64", cpu_model=cpu_model())
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
@@ -262,7 +288,9 @@ def main():
         "gbps": round(step_bytes / (full["us"] * 1e-6) / 1e9, 1),
         "hbm_frac": round(step_bytes / (full["us"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         "warm_us": round(full["warm_us"], 3),
+        "per_call_us": full["dist"],
         "mean": {"us": round(mean["us"], 3), "warm_us": round(mean["warm_us"], 3),
+                 "per_call_us": mean["dist"],
                  "gbps": round(step_bytes / (mean["us"] * 1e-6) / 1e9, 1),
                  "speedup_vs_full": round(full["us"] / mean["us"], 3)},
         "seq_scan": {"full_us": round(sfull["us"], 3), "mean_us": round(smean["us"], 3),
