@@ -255,27 +255,32 @@ constexpr int kComputeWaves = 12;  // G channels x Wv waves
 constexpr int kCopyWaves = 4;      // one per SIMD, copies only
 constexpr int kStageThreads = (kComputeWaves + kCopyWaves) * kWave;
 
+// The loop over a row's pieces is unrolled (at most kIt per wave) with
+// wave-uniform bounds, so issuing costs a few scalar instructions and one
+// lane-offset add per copy. Lanes past the row's end copy nothing.
+template <int kBytes, typename Tin>
+__device__ __forceinline__ void stage_pieces(const Tin* src, Tin* dst, int len, int issuer,
+                                             int lane) {
+    constexpr int kPer = kBytes / static_cast<int>(sizeof(Tin));  // elements per lane-piece
+    constexpr int kSpan = kWave * kPer;                            // per wave-instruction
+    constexpr int kIt = (kStageMax + kCopyWaves * kSpan - 1) / (kCopyWaves * kSpan);
+    const int jl = lane * kPer;
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        const int base = (issuer + it * kCopyWaves) * kSpan;
+        if (base >= len) break;
+        if (base + jl < len)
+            __builtin_amdgcn_global_load_lds(src + base + jl, dst + base, kBytes, 0, 0);
+    }
+}
+
 template <typename Tin>
 __device__ __forceinline__ void stage_row(const Tin* row, Tin* dst, int cs, int len, bool vec4,
                                           int issuer, int lane) {
-    constexpr int kEl = static_cast<int>(sizeof(Tin));
-    if (vec4) {
-        constexpr int kPer = 16 / kEl;          // elements per lane-piece
-        constexpr int kSpan = kWave * kPer;     // elements per wave-instruction
-        for (int base = issuer * kSpan; base < len; base += kCopyWaves * kSpan) {
-            const int j = base + lane * kPer;
-            if (j < len)
-                __builtin_amdgcn_global_load_lds(row + cs + j, dst + base, 16, 0, 0);
-        }
-    } else {
-        constexpr int kPer = 4 / kEl;
-        constexpr int kSpan = kWave * kPer;
-        for (int base = issuer * kSpan; base < len; base += kCopyWaves * kSpan) {
-            const int j = base + lane * kPer;
-            if (j < len)
-                __builtin_amdgcn_global_load_lds(row + cs + j, dst + base, 4, 0, 0);
-        }
-    }
+    if (vec4)
+        stage_pieces<16>(row + cs, dst, len, issuer, lane);
+    else
+        stage_pieces<4>(row + cs, dst, len, issuer, lane);
 }
 
 // Row n0 + s of B or C for pair step p (chunk p / pairs, state
