@@ -51,6 +51,10 @@ def _load():
     lib.oracle_cross_merge_f32.argtypes = [P, P, I64, I64, I64, I64]
     lib.oracle_cross_merge_bf16.argtypes = [P, P, I64, I64, I64, I64]
     lib.oracle_f32_to_bf16.argtypes = [P, P, I64]
+    lib.oracle_discrete_scan.argtypes = [P, P, P, P, I64, I64, I64, P, ctypes.c_int]
+    lib.oracle_discrete_scan.restype = None
+    lib.oracle_channel_mean.argtypes = [P, I64, I64, I64, P, ctypes.c_int]
+    lib.oracle_channel_mean.restype = None
     lib.oracle_max_threads.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -117,6 +121,33 @@ def mean_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
     if sel is None:
         return y.reshape(np.shape(u))
     return y
+
+
+def discrete_scan(abar, bu, C, skip=None, nthreads: int = 0) -> np.ndarray:
+    """One-state scan on materialised inputs in fp64.
+
+    abar, bu, skip: [batch, Dc, L] (skip may be None); C: [batch, L].
+    Returns y [batch, Dc, L] with h_t = abar_t h_{t-1} + bu_t, y_t = C_t h_t + skip_t.
+    """
+    lib = _load()
+    abar, bu, C, skip = _f32(abar), _f32(bu), _f32(C), _f32(skip)
+    batch, Dc, L = abar.shape
+    assert bu.shape == abar.shape and C.shape == (batch, L)
+    assert skip is None or skip.shape == abar.shape
+    y = np.empty((batch, Dc, L), dtype=np.float64)
+    lib.oracle_discrete_scan(_ptr(abar), _ptr(bu), _ptr(C), _ptr(skip), batch, Dc, L, _ptr(y),
+                             int(nthreads))
+    return y
+
+
+def channel_mean(x, nthreads: int = 0) -> np.ndarray:
+    """T of eq. 9 on a materialised input: x [batch, Dc, L] -> [batch, L] (fp64)."""
+    lib = _load()
+    x = _f32(x)
+    batch, Dc, L = x.shape
+    xm = np.empty((batch, L), dtype=np.float64)
+    lib.oracle_channel_mean(_ptr(x), batch, Dc, L, _ptr(xm), int(nthreads))
+    return xm
 
 
 def cross_scan(x: np.ndarray) -> np.ndarray:

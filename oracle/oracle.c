@@ -185,6 +185,55 @@ void oracle_mean_scan(const float* u, const float* delta, const float* A, const 
 }
 
 /*
+ * Scan on materialised, discretised inputs with one state (the decomposition
+ * of the paper's kernel experiments, Appendix D and Table 1: discretisation
+ * runs outside the kernel, which only walks the recurrence of eq. 3; the
+ * computational-complexity appendix counts the scan per (d, t) with N = 1).
+ * Tensors (row-major):
+ *   abar, bu : [batch, Dc, L]     C : [batch, L]     skip : [batch, Dc, L] or NULL
+ * For each (b, d):
+ *   h_{-1} = 0
+ *   h_t    = abar[b, d, t] * h_{t-1} + bu[b, d, t]
+ *   y_t    = C[b, t] * h_t + skip[b, d, t]
+ * y receives [batch, Dc, L].
+ */
+void oracle_discrete_scan(const float* abar, const float* bu, const float* C, const float* skip,
+                          int64_t batch, int64_t Dc, int64_t L, double* y, int nthreads) {
+    set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t s = 0; s < batch * Dc; ++s) {
+        const int64_t b = s / Dc;
+        const float* as = abar + s * L;
+        const float* bs = bu + s * L;
+        const float* ks = skip ? skip + s * L : NULL;
+        const float* cs = C + b * L;
+        double h = 0.0;
+        for (int64_t t = 0; t < L; ++t) {
+            h = (double)as[t] * h + (double)bs[t];
+            y[s * L + t] = (double)cs[t] * h + (ks ? (double)ks[t] : 0.0);
+        }
+    }
+}
+
+/*
+ * The transform T of eq. 9 on a materialised input: the mean over the inner
+ * channel axis (Section 2.2), summed in index order.
+ *   x : [batch, Dc, L]  ->  xm : [batch, L],  xm[b, t] = (1/Dc) sum_d x[b, d, t]
+ */
+void oracle_channel_mean(const float* x, int64_t batch, int64_t Dc, int64_t L, double* xm,
+                         int nthreads) {
+    set_threads(nthreads);
+#pragma omp parallel for schedule(static)
+    for (int64_t b = 0; b < batch; ++b) {
+        for (int64_t t = 0; t < L; ++t) {
+            double acc = 0.0;
+            for (int64_t d = 0; d < Dc; ++d) acc += (double)x[(b * Dc + d) * L + t];
+            xm[b * L + t] = acc / (double)Dc;
+        }
+    }
+}
+
+/*
  * Cross-scan position maps for an H x W map, pixel p = h*W + w:
  *   pi_0(h, w) = h*W + w          (row-major)
  *   pi_1(h, w) = w*H + h          (column-major)

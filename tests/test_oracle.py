@@ -420,3 +420,84 @@ def test_degenerate_sizes():
     ref = float(c["C"].ravel()[0]) * dl * float(c["B"].ravel()[0]) * float(c["u"].ravel()[0]) \
         + float(c["D"][0]) * float(c["u"].ravel()[0])
     assert abs(y.ravel()[0] - ref) <= 1e-14 * max(1.0, abs(ref))
+
+
+# ------------------------------------------- scan on materialised inputs (N = 1)
+# The decomposition of the paper's kernel experiments (Appendix D, Table 1):
+# discretisation outside, a one-state scan inside; T applied beforehand.
+
+def _discrete_case(seed, batch=2, Dc=3, L=17, with_skip=True):
+    rng = np.random.default_rng(seed)
+    abar = rng.uniform(0.3, 1.0, size=(batch, Dc, L)).astype(np.float32)
+    bu = rng.standard_normal((batch, Dc, L)).astype(np.float32)
+    C = rng.standard_normal((batch, L)).astype(np.float32)
+    skip = rng.standard_normal((batch, Dc, L)).astype(np.float32) if with_skip else None
+    return abar, bu, C, skip
+
+
+def test_discrete_scan_is_full_scan_with_one_state():
+    """With abar = exp(Delta A), bu = Delta B u and skip = D u formed outside,
+    the one-state scan is the (independently pinned) full scan at N = 1."""
+    c = rand_case(40, batch=2, K=1, Dc=3, L=13, N=1)
+    y_full = run_full(c)[:, 0]  # [batch, Dc, L]
+    dl = timescale_np(c["delta"], c["dt_bias"], c["softplus"], 1, 3)[:, 0]
+    A = c["A"][:, 0].astype(np.float64).reshape(1, 3, 1)
+    abar = np.exp(dl * A).astype(np.float32)
+    bu = (dl * c["B"][:, 0, 0][:, None, :] * c["u"][:, 0]).astype(np.float32)
+    skip = (c["D"].astype(np.float64).reshape(1, 3, 1) * c["u"][:, 0]).astype(np.float32)
+    y = oracle.discrete_scan(abar, bu, c["C"][:, 0, 0], skip)
+    # inputs rounded to fp32 on the way in: agreement to fp32 input precision
+    np.testing.assert_allclose(y, y_full, rtol=2e-6, atol=2e-6)
+
+
+def test_discrete_scan_geometric_series():
+    """Constant a, b, C = 1, no skip: h_t = b (1 - a^{t+1}) / (1 - a)."""
+    L = 40
+    a, b = 0.8125, 0.375  # exact in fp32
+    abar = np.full((1, 2, L), a, np.float32)
+    bu = np.full((1, 2, L), b, np.float32)
+    C = np.ones((1, L), np.float32)
+    y = oracle.discrete_scan(abar, bu, C)
+    t = np.arange(L)
+    ref = b * (1.0 - a ** (t + 1)) / (1.0 - a)
+    np.testing.assert_allclose(y[0, 0], ref, rtol=1e-14, atol=0)
+    np.testing.assert_allclose(y[0, 1], ref, rtol=1e-14, atol=0)
+
+
+def test_discrete_scan_product_form_brute_force():
+    """h_t = sum_{s<=t} (prod_{r=s+1..t} a_r) b_s, y_t = C_t h_t + skip_t."""
+    abar, bu, C, skip = _discrete_case(41, batch=2, Dc=2, L=11)
+    y = oracle.discrete_scan(abar, bu, C, skip)
+    a64, b64 = abar.astype(np.float64), bu.astype(np.float64)
+    for bb in range(2):
+        for d in range(2):
+            for t in range(11):
+                h = sum(np.prod(a64[bb, d, s + 1:t + 1]) * b64[bb, d, s] for s in range(t + 1))
+                ref = float(C[bb, t]) * h + float(skip[bb, d, t])
+                assert abs(y[bb, d, t] - ref) <= 1e-12 * max(1.0, abs(ref))
+
+
+def test_channel_mean_matches_numpy():
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal((3, 7, 19)).astype(np.float32)
+    np.testing.assert_allclose(oracle.channel_mean(x), x.astype(np.float64).mean(axis=1),
+                               rtol=1e-14, atol=1e-15)
+
+
+def test_scan_of_channel_means_is_mean_of_scans_when_decay_shared():
+    """Linearity: with abar the same on every channel, the one-channel scan of
+    T(bu) (and T(skip)) is the channel mean of the per-channel scans."""
+    abar, bu, C, skip = _discrete_case(43, batch=2, Dc=5, L=23)
+    abar[...] = abar[:, :1, :]
+    y = oracle.discrete_scan(abar, bu, C, skip)
+    am = oracle.channel_mean(abar).astype(np.float32)[:, None, :]
+    bm = oracle.channel_mean(bu).astype(np.float32)[:, None, :]
+    sm = oracle.channel_mean(skip).astype(np.float32)[:, None, :]
+    ym = oracle.discrete_scan(am, bm, C, sm)[:, 0]
+    np.testing.assert_allclose(ym, y.mean(axis=1), rtol=1e-6, atol=1e-6)
+
+
+def test_discrete_scan_degenerate_sizes():
+    abar, bu, C, _ = _discrete_case(44, batch=1, Dc=1, L=1, with_skip=False)
+    y = oracle.discrete_scan(abar, bu, C)
+    assert y.shape == (1, 1, 1) and y[0, 0, 0] == float(C[0, 0]) * float(bu[0, 0, 0])
