@@ -159,6 +159,41 @@ vmb_status vmb_mean_scan_fwd(const void* u, const void* delta, const float* A, c
                              void* workspace, size_t workspace_bytes, vmb_stream_t stream);
 
 /*
+ * One-state scan on materialised, discretised inputs: the decomposition of
+ * the paper's kernel experiments (Appendix D: the kernel only walks the
+ * recurrence of eq. 3, discretisation runs outside it; Table 1 shapes, one
+ * state per (d, t) as in the computational-complexity appendix). For every
+ * (b, d):
+ *   h_{-1} = 0
+ *   h_t    = abar[b,d,t] * h_{t-1} + bu[b,d,t]
+ *   y_t    = C[b,t] * h_t + skip[b,d,t]
+ * With channels = 1 and inputs reduced by vmb_channel_mean, the same call is
+ * the VMeanba kernel of those experiments (the scan of T(Abar), T(Bbar u)).
+ *
+ *   abar, bu : float32, [batch, channels, L]
+ *   C        : float32, [batch, L]
+ *   skip     : float32, [batch, channels, L] or NULL (treated as 0)
+ *   y        : float32, [batch, channels, L] (output)
+ * Binary32 state. Errors: VMB_ERR_NULL (abar, bu, C or y), VMB_ERR_SHAPE
+ * (a size < 1 or too large), VMB_ERR_ALIGN (a base not 16-byte aligned),
+ * VMB_ERR_ALIAS (y overlaps an input).
+ */
+vmb_status vmb_discrete_scan(const float* abar, const float* bu, const float* C,
+                             const float* skip, float* y, int64_t batch, int64_t channels,
+                             int64_t L, vmb_stream_t stream);
+
+/*
+ * The transform T of eq. 9 on a materialised input (Section 2.2: the mean
+ * over the inner channel axis):
+ *   xm[b, t] = (1 / channels) * sum_{d = 0 .. channels-1} x[b, d, t]
+ *   x  : float32, [batch, channels, L];  xm : float32, [batch, L] (output)
+ * Binary32 sums in a fixed order (deterministic). Errors as for
+ * vmb_discrete_scan.
+ */
+vmb_status vmb_channel_mean(const float* x, float* xm, int64_t batch, int64_t channels,
+                            int64_t L, vmb_stream_t stream);
+
+/*
  * Bytes of device workspace the scan of the given shape needs
  * (mean_variant = 0: vmb_selective_scan_fwd, 1: vmb_mean_scan_fwd).
  * Returns 0 when none is needed and SIZE_MAX for an invalid shape.

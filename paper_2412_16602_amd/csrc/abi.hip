@@ -91,6 +91,22 @@ size_t vmb_scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int6
     return scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout);
 }
 
+vmb_status vmb_discrete_scan(const float* abar, const float* bu, const float* C,
+                             const float* skip, float* y, int64_t batch, int64_t channels,
+                             int64_t L, vmb_stream_t stream) {
+    const vmb_status st = validate_discrete(abar, bu, C, skip, y, batch, channels, L);
+    if (st != VMB_OK) return st;
+    return launch_discrete_scan(abar, bu, C, skip, y, batch, channels, L,
+                                static_cast<hipStream_t>(stream));
+}
+
+vmb_status vmb_channel_mean(const float* x, float* xm, int64_t batch, int64_t channels,
+                            int64_t L, vmb_stream_t stream) {
+    const vmb_status st = validate_channel_mean(x, xm, batch, channels, L);
+    if (st != VMB_OK) return st;
+    return launch_channel_mean(x, xm, batch, channels, L, static_cast<hipStream_t>(stream));
+}
+
 const char* vmb_status_string(vmb_status s) {
     switch (s) {
         case VMB_OK: return "ok";

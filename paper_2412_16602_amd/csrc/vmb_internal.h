@@ -36,6 +36,10 @@ struct ScanArgs {
 vmb_status validate_cross(const void* in, const void* out, int64_t batch, int64_t channels,
                           int64_t H, int64_t W, vmb_dtype dt, bool unfold);
 vmb_status validate_scan(const ScanArgs& a, int mean_variant);
+vmb_status validate_discrete(const float* abar, const float* bu, const float* C, const float* skip,
+                             const float* y, int64_t batch, int64_t channels, int64_t L);
+vmb_status validate_channel_mean(const float* x, const float* xm, int64_t batch, int64_t channels,
+                                 int64_t L);
 size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                             int64_t L, int64_t N, vmb_layout layout);
 
@@ -95,6 +99,12 @@ vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t ch
                               int64_t H, int64_t W, vmb_dtype in_dt, vmb_dtype out_dt,
                               hipStream_t s);
 vmb_status launch_full_scan(const ScanArgs& a);
+// One-state scan on materialised inputs and the channel mean (scan_discrete.hip).
+vmb_status launch_discrete_scan(const float* abar, const float* bu, const float* C,
+                                const float* skip, float* y, int64_t batch, int64_t channels,
+                                int64_t L, hipStream_t s);
+vmb_status launch_channel_mean(const float* x, float* xm, int64_t batch, int64_t channels,
+                               int64_t L, hipStream_t s);
 // Positions-over-lanes full scan (N == 16); writes sequence-layout output to
 // y_seq (a.y for the sequence layout, the fp32 workspace for the 2-D one).
 vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq);

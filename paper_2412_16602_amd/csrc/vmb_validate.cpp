@@ -62,6 +62,35 @@ vmb_status validate_cross(const void* in, const void* out, int64_t batch, int64_
     return VMB_OK;
 }
 
+vmb_status validate_discrete(const float* abar, const float* bu, const float* C, const float* skip,
+                             const float* y, int64_t batch, int64_t channels, int64_t L) {
+    if (!abar || !bu || !C || !y) return VMB_ERR_NULL;
+    if (batch < 1 || channels < 1 || L < 1 || L > kMaxRow) return VMB_ERR_SHAPE;
+    const int64_t n = prod({batch, channels, L});
+    const int64_t nc = prod({batch, L});
+    if (n < 0 || nc < 0) return VMB_ERR_SHAPE;
+    if (!aligned(abar, 16) || !aligned(bu, 16) || !aligned(C, 16) || !aligned(y, 16) ||
+        (skip && !aligned(skip, 16)))
+        return VMB_ERR_ALIGN;
+    const Range ry = range_of(y, n, 4);
+    if (overlap(ry, range_of(abar, n, 4)) || overlap(ry, range_of(bu, n, 4)) ||
+        overlap(ry, range_of(C, nc, 4)) || (skip && overlap(ry, range_of(skip, n, 4))))
+        return VMB_ERR_ALIAS;
+    return VMB_OK;
+}
+
+vmb_status validate_channel_mean(const float* x, const float* xm, int64_t batch, int64_t channels,
+                                 int64_t L) {
+    if (!x || !xm) return VMB_ERR_NULL;
+    if (batch < 1 || channels < 1 || L < 1 || L > kMaxRow) return VMB_ERR_SHAPE;
+    const int64_t n = prod({batch, channels, L});
+    const int64_t nm = prod({batch, L});
+    if (n < 0 || nm < 0) return VMB_ERR_SHAPE;
+    if (!aligned(x, 16) || !aligned(xm, 16)) return VMB_ERR_ALIGN;
+    if (overlap(range_of(xm, nm, 4), range_of(x, n, 4))) return VMB_ERR_ALIAS;
+    return VMB_OK;
+}
+
 size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                             int64_t L, int64_t N, vmb_layout layout) {
     if (batch < 1 || K < 1 || channels < 1 || L < 1 || N < 1) return SIZE_MAX;

@@ -57,6 +57,10 @@ def load_library():
         fn = getattr(lib, name)
         fn.argtypes = scan
         fn.restype = I
+    lib.vmb_discrete_scan.argtypes = [P, P, P, P, P, I64, I64, I64, P]
+    lib.vmb_discrete_scan.restype = I
+    lib.vmb_channel_mean.argtypes = [P, P, I64, I64, I64, P]
+    lib.vmb_channel_mean.restype = I
     lib.vmb_scan_workspace_bytes.argtypes = [I, I64, I64, I64, I64, I64, I]
     lib.vmb_scan_workspace_bytes.restype = ctypes.c_size_t
     lib.vmb_status_string.argtypes = [I]
@@ -202,3 +206,34 @@ def vmb_mean_scan_fwd(u, delta, A, B, C, D, dt_bias, delta_softplus, y,
     """VMeanba channel-mean scan; shapes as in include/vmb.h. Returns y."""
     return _scan("vmb_mean_scan_fwd", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
                  y, layout, workspace, stream)
+
+
+def vmb_discrete_scan(abar: torch.Tensor, bu: torch.Tensor, C: torch.Tensor,
+                      skip: Optional[torch.Tensor], y: torch.Tensor, stream=None) -> torch.Tensor:
+    """One-state scan on materialised inputs (float32).
+
+    abar, bu, skip, y: [batch, channels, L] (skip may be None); C: [batch, L].
+    h_t = abar_t h_{t-1} + bu_t, y_t = C_t h_t + skip_t.
+    """
+    lib = load_library()
+    batch, channels, L = abar.shape
+    for t, name in ((bu, "bu"), (y, "y")) + (((skip, "skip"),) if skip is not None else ()):
+        if tuple(t.shape) != (batch, channels, L):
+            raise ValueError(f"{name} shape {tuple(t.shape)} != {(batch, channels, L)}")
+    if tuple(C.shape) != (batch, L):
+        raise ValueError(f"C shape {tuple(C.shape)} != {(batch, L)}")
+    _check(lib.vmb_discrete_scan(_f32(abar, "abar"), _f32(bu, "bu"), _f32(C, "C"),
+                                 _f32(skip, "skip"), _f32(y, "y"), batch, channels, L,
+                                 _stream(stream)), "vmb_discrete_scan")
+    return y
+
+
+def vmb_channel_mean(x: torch.Tensor, xm: torch.Tensor, stream=None) -> torch.Tensor:
+    """T of eq. 9: x [batch, channels, L] -> xm [batch, L], the channel mean (float32)."""
+    lib = load_library()
+    batch, channels, L = x.shape
+    if tuple(xm.shape) != (batch, L):
+        raise ValueError(f"xm shape {tuple(xm.shape)} != {(batch, L)}")
+    _check(lib.vmb_channel_mean(_f32(x, "x"), _f32(xm, "xm"), batch, channels, L,
+                                _stream(stream)), "vmb_channel_mean")
+    return xm

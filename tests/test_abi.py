@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol(lib):
     names = vmb.declared_symbols()
     assert set(names) >= {"vmb_cross_scan", "vmb_cross_merge", "vmb_selective_scan_fwd",
                           "vmb_mean_scan_fwd", "vmb_scan_workspace_bytes", "vmb_status_string",
-                          "vmb_abi_version"}
+                          "vmb_abi_version", "vmb_discrete_scan", "vmb_channel_mean"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -112,6 +112,34 @@ def test_cross_rejects(lib, fn, unfold):
     if not unfold:
         # merge input is the 4-direction tensor (384 B): an output 256 B in overlaps it
         assert f(P(0), P(0, 256), 1, 2, 3, 4, F32, None) == ALIAS
+
+
+def test_discrete_scan_rejects(lib):
+    f = lib.vmb_discrete_scan
+    # abar, bu, skip: [2, 3, 8] floats (192 B); C: [2, 8]
+    ok = dict(a=P(0), b=P(1), c=P(2), k=P(3), y=P(4), batch=2, ch=3, L=8)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["a"], a["b"], a["c"], a["k"], a["y"], a["batch"], a["ch"], a["L"], None)
+
+    assert call(a=None) == NULL and call(b=None) == NULL and call(c=None) == NULL
+    assert call(y=None) == NULL
+    assert call(batch=0) == SHAPE and call(ch=0) == SHAPE and call(L=-1) == SHAPE
+    assert call(L=1 << 31) == SHAPE
+    assert call(a=P(0, 4)) == ALIGN and call(k=P(3, 8)) == ALIGN and call(y=P(4, 4)) == ALIGN
+    assert call(y=P(0, 64)) == ALIAS and call(y=P(2, 48)) == ALIAS and call(y=P(3)) == ALIAS
+    # skip is optional
+    assert lib.vmb_discrete_scan(P(0), P(1), P(2), None, None, 2, 3, 8, None) == NULL
+
+
+def test_channel_mean_rejects(lib):
+    f = lib.vmb_channel_mean
+    assert f(None, P(1), 2, 3, 8, None) == NULL and f(P(0), None, 2, 3, 8, None) == NULL
+    assert f(P(0), P(1), 0, 3, 8, None) == SHAPE and f(P(0), P(1), 2, 3, 0, None) == SHAPE
+    assert f(P(0, 4), P(1), 2, 3, 8, None) == ALIGN and f(P(0), P(1, 8), 2, 3, 8, None) == ALIGN
+    assert f(P(0), P(0, 128), 2, 3, 8, None) == ALIAS
 
 
 def test_python_binding_refuses_cpu_tensors():

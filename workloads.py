@@ -155,3 +155,42 @@ def make_inputs(shape: Shape, layout: str = "seq", *, batch: Optional[int] = Non
 def custom_shape(batch: int, H: int, W: int, channels: int, N: int, dtype: str = "f32",
                  seed: int = 0, low_variance: bool = True, name: str = "custom") -> Shape:
     return Shape(name, batch, H, W, channels, N, dtype, seed, low_variance)
+
+
+# ------------------------------------------------ materialised scan inputs
+# The shapes of the paper's kernel experiments (Appendix D, Table 1): batch
+# 128, one state, (inner dimension, sequence length) per VMamba stage, for the
+# Tiny/Small and Base backbones.
+TABLE1_SHAPES = [
+    ("tiny_small", 384, 3136), ("tiny_small", 768, 784), ("tiny_small", 1536, 196),
+    ("tiny_small", 3072, 49),
+    ("base", 512, 3136), ("base", 1024, 784), ("base", 2048, 196), ("base", 4096, 49),
+]
+TABLE1_BATCH = 128
+
+
+@dataclasses.dataclass
+class DiscreteInputs:
+    abar: np.ndarray  # [batch, channels, L]
+    bu: np.ndarray    # [batch, channels, L]
+    C: np.ndarray     # [batch, L]
+    skip: Optional[np.ndarray]  # [batch, channels, L] or None
+
+
+def make_discrete_inputs(batch: int, channels: int, L: int, seed: int,
+                         with_skip: bool = False) -> DiscreteInputs:
+    """Materialised one-state scan inputs, drawn directly (no discretisation
+    is computed here): abar uniform in [e^-0.1, e^-0.001] (the decays exp(-dt)
+    of dt in [1e-3, 1e-1] with A = -1), bu ~ N(0, 0.05^2) with the low
+    cross-channel variance of the SS2D activations (a per-(b, t) base plus
+    channel noise of one tenth its size), C ~ N(0, 1), skip ~ N(0, 1).
+    Draw order: abar, bu base, bu noise, C, skip (PCG64, float32)."""
+    rng = np.random.default_rng(seed)
+    lo, hi = math.exp(-0.1), math.exp(-0.001)
+    abar = rng.uniform(lo, hi, size=(batch, channels, L)).astype(np.float32)
+    base = rng.standard_normal((batch, 1, L), dtype=np.float32)
+    noise = rng.standard_normal((batch, channels, L), dtype=np.float32)
+    bu = (np.float32(0.05) * (base + np.float32(0.1) * noise)).astype(np.float32)
+    C = rng.standard_normal((batch, L), dtype=np.float32)
+    skip = rng.standard_normal((batch, channels, L), dtype=np.float32) if with_skip else None
+    return DiscreteInputs(abar=abar, bu=bu, C=C, skip=skip)
