@@ -233,6 +233,74 @@ def cpu_baseline(budget_s: float):
                        f"192 channels, N=16, fp64", cpu_model=cpu_model())
 
 
+# The paper's Table 1 times of the original (all-channel) kernel on its own
+# GPU (an NVIDIA RTX A6000), in ms, for context only.
+PAPER_TABLE1_MS = {("tiny_small", 384, 3136): 5.46, ("tiny_small", 768, 784): 2.23,
+                   ("tiny_small", 1536, 196): 1.10, ("tiny_small", 3072, 49): 0.71,
+                   ("base", 512, 3136): 5.86, ("base", 1024, 784): 2.94,
+                   ("base", 2048, 196): 1.47, ("base", 4096, 49): 0.93}
+
+
+def table1_bench(steps: int, warmup: int):
+    """The decomposition of the paper's kernel experiments (Table 1 shapes,
+    batch 128, one state): the scan on materialised inputs over all channels,
+    and the VMeanba path (T on both inputs, then the scan at one channel).
+    Inputs are drawn on the GPU (uniform decays, normal bu and C)."""
+    import torch
+
+    from paper_2412_16602_amd import vmb
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    B = workloads.TABLE1_BATCH
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps
+
+    rows = []
+    for backbone, D, L in workloads.TABLE1_SHAPES:
+        abar = 0.9 + 0.099 * torch.rand(B, D, L, device=dev, generator=g)
+        bu = 0.05 * torch.randn(B, D, L, device=dev, generator=g)
+        C = torch.randn(B, L, device=dev, generator=g)
+        y = torch.empty_like(abar)
+        am = torch.empty(B, 1, L, device=dev)
+        bm = torch.empty(B, 1, L, device=dev)
+        y1 = torch.empty(B, 1, L, device=dev)
+        full_us = timed(lambda: vmb.vmb_discrete_scan(abar, bu, C, None, y, stream=stream))
+        red_us = timed(lambda: (vmb.vmb_channel_mean(abar, am.view(B, L), stream=stream),
+                                vmb.vmb_channel_mean(bu, bm.view(B, L), stream=stream)))
+        d1_us = timed(lambda: vmb.vmb_discrete_scan(am, bm, C, None, y1, stream=stream))
+        full_bytes = B * D * L * 12 + B * L * 4
+        red_bytes = 2 * (B * D * L * 4 + B * L * 4)
+        rows.append({
+            "backbone": backbone, "channels": D, "L": L, "batch": B,
+            "full_us": round(full_us, 2),
+            "full_gbps": round(full_bytes / (full_us * 1e-6) / 1e9, 1),
+            "full_hbm_frac": round(full_bytes / (full_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "mean_scan_d1_us": round(d1_us, 2),
+            "speedup_scan": round(full_us / d1_us, 1),
+            "mean_reduce_us": round(red_us, 2),
+            "reduce_gbps": round(red_bytes / (red_us * 1e-6) / 1e9, 1),
+            "paper_original_ms_a6000": PAPER_TABLE1_MS[(backbone, D, L)],
+        })
+        del abar, bu, C, y, am, bm, y1
+        torch.cuda.empty_cache()
+    return {"metric": "one-state scan on materialised inputs, Table 1 shapes (us/call)",
+            "unit": "us/call", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -253,6 +321,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calibrate", action="store_true",
                     help="run a 256 MiB copy first (counter calibration dispatch)")
+    ap.add_argument("--table1", action="store_true",
+                    help="after the main line, print a second JSON line: the one-state scan "
+                         "on materialised inputs at the paper's Table 1 shapes")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this SS2D scan library runs on a single "
@@ -311,6 +382,8 @@ def main():
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
     print(json.dumps(out), flush=True)
+    if args.table1:
+        print(json.dumps(table1_bench(max(5, args.steps // 10), 3)), flush=True)
 
 
 if __name__ == "__main__":
