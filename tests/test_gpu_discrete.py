@@ -26,9 +26,18 @@ def _run_scan(inp: workloads.DiscreteInputs):
     return y.cpu().numpy().astype(np.float64)
 
 
+# sequences under 8 positions take a 16-lane row each; up to 256 positions
+# several whole sequences share a wave as one flat run (Q of them: 2 for
+# (2, 2048, 100), 6 for (1, 12288, 28), 4 for the small odd L, crossing batch
+# elements when Q does not divide the channels); longer ones take one wave
+# each when there are at least 2048 of them ((4, 1024, 600)), else one
+# workgroup each with the chunks spread over up to 16 waves (one to three
+# groups of 16 chunks)
 @pytest.mark.parametrize("batch,channels,L", [
-    (1, 1, 1), (2, 3, 7), (1, 2, 512), (1, 2, 513), (2, 3, 1000), (1, 1, 3136), (3, 2, 49),
-    (2, 5, 196), (1, 3, 1026), (1, 1, 4099)])
+    (1, 1, 1), (2, 3, 7), (5, 3, 4), (1, 1, 8), (3, 5, 9), (4, 3, 30), (3, 3, 50), (2, 7, 49),
+    (1, 2, 512), (1, 2, 513), (2, 3, 1000), (1, 1, 3136), (3, 2, 49), (2, 5, 196), (1, 3, 1026),
+    (1, 1, 4099), (5, 7, 64), (3, 11, 65), (2, 9, 256), (2, 13, 100), (1, 1, 257),
+    (2, 2048, 100), (1, 12288, 28), (4, 1024, 600), (1, 2, 20000), (2, 1, 8193)])
 @pytest.mark.parametrize("with_skip", [False, True])
 def test_discrete_scan_small(batch, channels, L, with_skip):
     log(f"discrete scan {batch}x{channels}x{L} skip={with_skip}")
@@ -38,7 +47,12 @@ def test_discrete_scan_small(batch, channels, L, with_skip):
     assert_close(got, ref, **FP32_TOL, what=f"discrete scan {batch}x{channels}x{L}")
 
 
-@pytest.mark.parametrize("batch,channels,L", [(1, 1, 5), (2, 7, 33), (3, 64, 1000), (1, 9, 4096)])
+# rows of lcm(L, 4) elements (one tile folded to positions for L = 49, 98,
+# 50; whole position rows for L % 4 == 0), element rows otherwise; 1 to 16
+# waves splitting the rows, with and without a remainder
+@pytest.mark.parametrize("batch,channels,L", [
+    (1, 1, 5), (2, 7, 33), (3, 64, 1000), (1, 9, 4096), (2, 12, 49), (3, 6, 98), (2, 5, 130),
+    (2, 40, 50), (1, 3, 1001), (4, 700, 49), (2, 16, 3136), (2, 333, 196), (1, 6, 2)])
 def test_channel_mean_small(batch, channels, L):
     log(f"channel mean {batch}x{channels}x{L}")
     rng = np.random.default_rng(batch * 1000 + L)
@@ -87,3 +101,31 @@ def test_table1_shapes_sampled(backbone, channels, L):
         ref = oracle.discrete_scan(inp.abar[b:b + 1, d:d + 1], inp.bu[b:b + 1, d:d + 1],
                                    inp.C[b:b + 1])
         assert_close(y[b, d].cpu().numpy(), ref[0, 0], **FP32_TOL, what=f"({b}, {d})")
+
+
+def test_graph_replay_matches_eager():
+    """The calls captured in a HIP graph (as the Table 1 timing does): every
+    replay, with eager work between, equals the eager result bit for bit."""
+    inp = workloads.make_discrete_inputs(2, 40, 196, seed=9)
+    a, b, c = map(_up, (inp.abar, inp.bu, inp.C))
+    y_ref = torch.empty_like(a)
+    am_ref = torch.empty(2, 196, device=dev())
+    vmb.vmb_discrete_scan(a, b, c, None, y_ref)
+    vmb.vmb_channel_mean(a, am_ref)
+    torch.cuda.synchronize()
+    y = torch.empty_like(a)
+    am = torch.empty(2, 196, device=dev())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        st = torch.cuda.current_stream()
+        vmb.vmb_discrete_scan(a, b, c, None, y, stream=st)
+        vmb.vmb_channel_mean(a, am, stream=st)
+    for i in range(3):
+        y.fill_(float("nan"))
+        am.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_ref), f"replay {i}: scan"
+        assert torch.equal(am, am_ref), f"replay {i}: channel mean"
+        vmb.vmb_discrete_scan(b, a, c, None, y_ref.clone())  # eager work in between
+        torch.cuda.synchronize()
