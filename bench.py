@@ -31,6 +31,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -245,9 +246,10 @@ def table1_bench(steps: int, warmup: int):
     """The decomposition of the paper's kernel experiments (Table 1 shapes,
     batch 128, one state): the scan on materialised inputs over all channels,
     and the VMeanba path (T on both inputs, then the scan at one channel).
-    Inputs are drawn on the GPU (uniform decays, normal bu and C); the
-    one-channel scan reads the reduced inputs the reduce has just written, as
-    it would in use."""
+    Inputs are drawn on the GPU with the distributions of
+    workloads.make_discrete_inputs (uniform decays, low cross-channel
+    variance bu, normal C); the one-channel scan reads the reduced inputs
+    the reduce has just written, as it would in use."""
     import torch
 
     from paper_2412_16602_amd import vmb
@@ -288,9 +290,12 @@ def table1_bench(steps: int, warmup: int):
         set_bytes = B * D * L * 12
         n_sets = max(2, -(-ROTATE_BYTES // set_bytes))
         sets = []
+        lo, hi = math.exp(-0.1), math.exp(-0.001)
         for _ in range(n_sets):
-            abar = 0.9 + 0.099 * torch.rand(B, D, L, device=dev, generator=g)
-            bu = 0.05 * torch.randn(B, D, L, device=dev, generator=g)
+            # the distributions of workloads.make_discrete_inputs
+            abar = lo + (hi - lo) * torch.rand(B, D, L, device=dev, generator=g)
+            base = torch.randn(B, 1, L, device=dev, generator=g)
+            bu = 0.05 * (base + 0.1 * torch.randn(B, D, L, device=dev, generator=g))
             sets.append((abar, bu, torch.empty_like(abar)))
         C = torch.randn(B, L, device=dev, generator=g)
         am = torch.empty(B, 1, L, device=dev)
