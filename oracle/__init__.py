@@ -46,6 +46,8 @@ def _load():
     lib.oracle_full_scan.restype = None
     lib.oracle_mean_scan.argtypes = scan_args
     lib.oracle_mean_scan.restype = None
+    lib.oracle_mean_scan_opt.argtypes = scan_args[:15] + [ctypes.c_int] + scan_args[15:]
+    lib.oracle_mean_scan_opt.restype = None
     lib.oracle_cross_scan.argtypes = [P, P, I64, I64, I64, I64, I64]
     lib.oracle_cross_merge_f64.argtypes = [P, P, I64, I64, I64, I64]
     lib.oracle_cross_merge_f32.argtypes = [P, P, I64, I64, I64, I64]
@@ -74,7 +76,14 @@ def max_threads() -> int:
     return int(_load().oracle_max_threads())
 
 
-def _scan(fn_name, per_seq, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads):
+# reading variants of the mean scan (bit flags of oracle_mean_scan_opt)
+MEAN_SKIP_PER_CHANNEL = 1  # D u outside T, added per channel after the broadcast
+MEAN_RAW = 2               # T averages Delta, u and A before the discretisation
+MEAN_NO_BROADCAST = 4      # T^-1 left out: one reduced row per (batch, k)
+
+
+def _scan(fn_name, per_seq, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads,
+          options=None, rows=None):
     lib = _load()
     u, delta, A, B, C = map(_f32, (u, delta, A, B, C))
     D, dt_bias = _f32(D), _f32(dt_bias)
@@ -88,11 +97,13 @@ def _scan(fn_name, per_seq, u, delta, A, B, C, D, dt_bias, softplus, sel, nthrea
     else:
         sel_arr = np.ascontiguousarray(np.asarray(sel, dtype=np.int64))
         nsel = int(sel_arr.size)
-    shape = (nsel, L) if per_seq else (nsel, Dc, L)
+    shape = (nsel, L) if per_seq else (nsel, Dc if rows is None else rows, L)
     y = np.empty(shape, dtype=np.float64)
-    getattr(lib, fn_name)(_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(dt_bias),
-                          int(bool(softplus)), batch, K, Dc, L, N, _ptr(sel_arr), nsel, _ptr(y),
-                          int(nthreads))
+    args = [_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(dt_bias),
+            int(bool(softplus)), batch, K, Dc, L, N, _ptr(sel_arr), nsel]
+    if options is not None:
+        args.append(int(options))
+    getattr(lib, fn_name)(*args, _ptr(y), int(nthreads))
     return y
 
 
@@ -111,15 +122,27 @@ def full_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
 
 
 def mean_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
-              sel: Optional[Sequence[int]] = None, nthreads: int = 0) -> np.ndarray:
+              sel: Optional[Sequence[int]] = None, nthreads: int = 0,
+              options: int = 0) -> np.ndarray:
     """VMeanba channel-mean scan in fp64, output broadcast over channels.
 
     Returns [batch, K, Dc, L] (sel None) or [len(sel), Dc, L] for the flat
-    direction indices b*K + k in ``sel``.
+    direction indices b*K + k in ``sel``; with MEAN_NO_BROADCAST in
+    ``options`` one row per direction instead of Dc ([batch, K, 1, L]).
+    ``options`` 0 is the reading of the main path (means of the discretised
+    terms, the skip term reduced with them, broadcast output).
     """
-    y = _scan("oracle_mean_scan", False, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads)
+    if options == 0:
+        y = _scan("oracle_mean_scan", False, u, delta, A, B, C, D, dt_bias, softplus, sel,
+                  nthreads)
+    else:
+        assert not (options & MEAN_NO_BROADCAST and options & MEAN_SKIP_PER_CHANNEL)
+        rows = 1 if options & MEAN_NO_BROADCAST else None
+        y = _scan("oracle_mean_scan_opt", False, u, delta, A, B, C, D, dt_bias, softplus, sel,
+                  nthreads, options=options, rows=rows)
     if sel is None:
-        return y.reshape(np.shape(u))
+        batch, K, Dc, L = np.shape(u)
+        return y.reshape(batch, K, y.shape[1], L)
     return y
 
 

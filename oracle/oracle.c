@@ -134,28 +134,53 @@ void oracle_full_scan(const float* u, const float* delta, const float* A, const 
  *   h_t = Abar_mean[n, t] * h_{t-1} + B[n, t] * s_mean[t]
  *   ytilde_t = sum_n C[n, t] * h_t + r_mean[t]
  * and the broadcast y[d, t] = ytilde_t for every d.
+ *
+ * options (bit flags) select other readings of where T acts:
+ *   1  skip per channel: D u stays outside T, as in eq. 3 for each channel:
+ *        ytilde_t = sum_n C[n, t] h_t,  y[d, t] = ytilde_t + D[c] u_{d,t}
+ *   2  mean before the discretisation of eq. 4: T averages the timescale,
+ *      the input and the state matrix of the channels,
+ *        Delta_mean[t] = (1/Dc) sum_d Delta_{d,t},  u_mean[t] = (1/Dc) sum_d u_{d,t},
+ *        A_mean[n] = (1/Dc) sum_d A[c, n],
+ *      and the one-channel scan discretises those:
+ *        h_t = exp(Delta_mean[t] A_mean[n]) h_{t-1} + Delta_mean[t] B[n, t] u_mean[t]
+ *      (the skip term as above, r_mean or per channel)
+ *   4  no broadcast: T^-1 is left out and y receives [nsel, L], the reduced
+ *      output ytilde of each (b, k) (not with option 1)
  */
-void oracle_mean_scan(const float* u, const float* delta, const float* A, const float* Bm,
-                      const float* Cm, const float* Ds, const float* dt_bias, int softplus,
-                      int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,
-                      const int64_t* sel, int64_t nsel, double* y, int nthreads) {
+void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, const float* Bm,
+                          const float* Cm, const float* Ds, const float* dt_bias, int softplus,
+                          int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,
+                          const int64_t* sel, int64_t nsel, int options, double* y,
+                          int nthreads) {
+    const int skip_per_channel = (options & 1) != 0;
+    const int raw_mean = (options & 2) != 0;
+    const int broadcast = (options & 4) == 0;
     set_threads(nthreads);
     if (!sel) nsel = batch * K;
 #pragma omp parallel
     {
         double* h = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
         double* abar = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        double* amean = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
 #pragma omp for schedule(dynamic, 1)
         for (int64_t i = 0; i < nsel; ++i) {
             const int64_t bk = sel ? sel[i] : i;
             const int64_t k = bk % K;
             const float* Bs = Bm + bk * N * L;
             const float* Cs = Cm + bk * N * L;
+            const double inv = 1.0 / (double)Dc;
+            /* mean state matrix of the direction's channels (option 2) */
+            for (int64_t n = 0; n < N; ++n) {
+                double sum = 0.0;
+                for (int64_t d = 0; d < Dc; ++d) sum += (double)A[(k * Dc + d) * N + n];
+                amean[n] = sum * inv;
+            }
             for (int64_t n = 0; n < N; ++n) h[n] = 0.0;
             for (int64_t t = 0; t < L; ++t) {
-                /* T: mean over the inner channel axis of the discretised inputs */
+                /* T: mean over the inner channel axis */
                 for (int64_t n = 0; n < N; ++n) abar[n] = 0.0;
-                double s_sum = 0.0, r_sum = 0.0;
+                double s_sum = 0.0, r_sum = 0.0, dl_sum = 0.0, u_sum = 0.0;
                 for (int64_t d = 0; d < Dc; ++d) {
                     const int64_t c = k * Dc + d;
                     const int64_t off = (bk * Dc + d) * L + t;
@@ -164,24 +189,54 @@ void oracle_mean_scan(const float* u, const float* delta, const float* A, const 
                     for (int64_t n = 0; n < N; ++n) abar[n] += exp(dl * (double)A[c * N + n]);
                     s_sum += dl * ut;
                     r_sum += (Ds ? (double)Ds[c] : 0.0) * ut;
+                    dl_sum += dl;
+                    u_sum += ut;
                 }
-                const double inv = 1.0 / (double)Dc;
-                const double s_mean = s_sum * inv;
-                const double r_mean = r_sum * inv;
+                const double r_mean = skip_per_channel ? 0.0 : r_sum * inv;
                 /* Mamba on the reduced (one-channel) inputs */
                 double acc = 0.0;
                 for (int64_t n = 0; n < N; ++n) {
-                    h[n] = (abar[n] * inv) * h[n] + (double)Bs[n * L + t] * s_mean;
+                    double a_n, bu_n;
+                    if (raw_mean) {
+                        /* eq. 4 applied to the means */
+                        const double dm = dl_sum * inv, um = u_sum * inv;
+                        a_n = exp(dm * amean[n]);
+                        bu_n = dm * (double)Bs[n * L + t] * um;
+                    } else {
+                        /* the means of the discretised terms */
+                        a_n = abar[n] * inv;
+                        bu_n = (double)Bs[n * L + t] * (s_sum * inv);
+                    }
+                    h[n] = a_n * h[n] + bu_n;
                     acc += (double)Cs[n * L + t] * h[n];
                 }
                 const double yt = acc + r_mean;
+                if (!broadcast) {
+                    y[i * L + t] = yt;
+                    continue;
+                }
                 /* T^-1: broadcast to every channel */
-                for (int64_t d = 0; d < Dc; ++d) y[(i * Dc + d) * L + t] = yt;
+                for (int64_t d = 0; d < Dc; ++d) {
+                    const int64_t c = k * Dc + d;
+                    const double own = skip_per_channel && Ds
+                                           ? (double)Ds[c] * (double)u[(bk * Dc + d) * L + t]
+                                           : 0.0;
+                    y[(i * Dc + d) * L + t] = yt + own;
+                }
             }
         }
+        free(amean);
         free(abar);
         free(h);
     }
+}
+
+void oracle_mean_scan(const float* u, const float* delta, const float* A, const float* Bm,
+                      const float* Cm, const float* Ds, const float* dt_bias, int softplus,
+                      int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,
+                      const int64_t* sel, int64_t nsel, double* y, int nthreads) {
+    oracle_mean_scan_opt(u, delta, A, Bm, Cm, Ds, dt_bias, softplus, batch, K, Dc, L, N, sel, nsel,
+                         0, y, nthreads);
 }
 
 /*

@@ -257,6 +257,88 @@ def test_mean_output_is_broadcast():
     assert np.all(y == y[:, :, :1, :])
 
 
+# ---------------------------------------------------------------- mean-scan reading variants
+
+SKIP1, RAW, NOBC = oracle.MEAN_SKIP_PER_CHANNEL, oracle.MEAN_RAW, oracle.MEAN_NO_BROADCAST
+
+
+def _identical_channels(c, K, Dc, N):
+    for key in ("u", "delta"):
+        c[key][...] = c[key][:, :, :1, :]
+    A = c["A"].reshape(K, Dc, N)
+    A[...] = A[:, :1, :]
+    for key in ("D", "dt_bias"):
+        v = c[key].reshape(K, Dc)
+        v[...] = v[:, :1]
+
+
+@pytest.mark.parametrize("options", [SKIP1, RAW, SKIP1 | RAW])
+def test_mean_variants_equal_full_when_channels_identical(options):
+    """With identical channels every reading of T is the identity on them:
+    each variant equals the full scan."""
+    c = rand_case(40 + options, batch=2, K=2, Dc=4, L=12, N=3)
+    _identical_channels(c, 2, 4, 3)
+    np.testing.assert_allclose(run_mean(c, options=options), run_full(c), rtol=1e-12, atol=1e-13)
+
+
+def test_mean_raw_is_full_scan_of_averaged_inputs():
+    """Mean before discretisation, softplus off: Delta is affine in delta, so
+    the mean timescale is that of the mean delta and mean bias; with D equal
+    over a direction's channels, mean(D u) = D mean(u). The reduced scan is
+    then the full scan of one channel fed the averaged u, delta, bias, A."""
+    K, Dc, N, L = 3, 5, 4, 14
+    c = rand_case(46, batch=2, K=K, Dc=Dc, L=L, N=N, softplus=False)
+    D = c["D"].reshape(K, Dc)
+    D[...] = D[:, :1]
+    y = run_mean(c, options=RAW)
+    avg = lambda a, axis: a.astype(np.float64).mean(axis=axis, keepdims=True)
+    one = dict(u=avg(c["u"], 2).astype(np.float32), delta=avg(c["delta"], 2).astype(np.float32),
+               A=avg(c["A"].reshape(K, Dc, N), 1).reshape(K, N).astype(np.float32),
+               B=c["B"], C=c["C"], D=D[:, 0].copy(),
+               dt_bias=avg(c["dt_bias"].reshape(K, Dc), 1).reshape(K).astype(np.float32),
+               softplus=False)
+    ref = run_full(one)  # [batch, K, 1, L]
+    # the averages are rounded to float32 to feed the full scan
+    np.testing.assert_allclose(y, np.broadcast_to(ref, y.shape), rtol=2e-5, atol=2e-6)
+
+
+def test_mean_raw_equals_discretised_mean_when_timescale_shared():
+    """If Delta and A do not vary over channels, exp(Delta A) is the same for
+    every channel and mean(Delta u) = Delta mean(u): both readings of T give
+    the same reduced scan."""
+    c = rand_case(47, batch=1, K=3, Dc=6, L=13, N=3)
+    c["delta"][...] = c["delta"][:, :, :1, :]
+    A = c["A"].reshape(3, 6, 3)
+    A[...] = A[:, :1, :]
+    v = c["dt_bias"].reshape(3, 6)
+    v[...] = v[:, :1]
+    np.testing.assert_allclose(run_mean(c, options=RAW), run_mean(c), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("raw", [0, RAW])
+def test_mean_skip_per_channel_averages_to_reduced_skip(raw):
+    """The per-channel skip D[c] u_d averages over the channels to r_mean, so
+    the channel mean of the per-channel-skip output is the reduced-skip output,
+    and the two differ channel by channel by D[c] u_d - r_mean."""
+    K, Dc = 2, 5
+    c = rand_case(48 + raw, batch=2, K=K, Dc=Dc, L=11, N=3)
+    y1 = run_mean(c, options=SKIP1 | raw)
+    y2 = run_mean(c, options=raw)
+    np.testing.assert_allclose(y1.mean(axis=2, keepdims=True), y2[:, :, :1], rtol=1e-12,
+                               atol=1e-13)
+    du = c["D"].astype(np.float64).reshape(1, K, Dc, 1) * c["u"].astype(np.float64)
+    np.testing.assert_allclose(y1 - du, y2 - du.mean(axis=2, keepdims=True), rtol=1e-12,
+                               atol=1e-13)
+
+
+@pytest.mark.parametrize("raw", [0, RAW])
+def test_mean_no_broadcast_is_one_row(raw):
+    c = rand_case(50 + raw, batch=2, K=2, Dc=4, L=10, N=2)
+    y = run_mean(c, options=NOBC | raw)
+    assert y.shape == (2, 2, 1, 10)
+    assert np.array_equal(y, run_mean(c, options=raw)[:, :, :1])
+
+
 # ---------------------------------------------------------------- P6 permutations
 
 @pytest.mark.parametrize("H,W", [(1, 1), (1, 5), (4, 1), (3, 3), (4, 6), (7, 7)])
