@@ -340,6 +340,68 @@ def table1_bench(steps: int, warmup: int):
             "rows": rows}
 
 
+def variants_bench(steps: int, warmup: int):
+    """The mean scan's reading variants (vmb_mean_scan_fwd_ex options) at the
+    stage-1 workload, next to the main reading: µs per call, inputs rotated
+    past the MALL, events on the launch stream."""
+    import torch
+
+    from paper_2412_16602_amd import vmb
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    shape = workloads.STAGE1
+    opts = {"main": 0, "skip_per_channel": vmb.VMB_MEAN_SKIP_PER_CHANNEL, "raw": vmb.VMB_MEAN_RAW,
+            "no_broadcast": vmb.VMB_MEAN_NO_BROADCAST,
+            "raw_no_broadcast": vmb.VMB_MEAN_RAW | vmb.VMB_MEAN_NO_BROADCAST}
+    rows = []
+    for layout in ("seq", "2d"):
+        inp = workloads.make_inputs(shape, layout)
+        g = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        lay = vmb.VMB_LAYOUT_2D if layout == "2d" else vmb.VMB_LAYOUT_SEQ
+        base = dict(u=g(inp.x if layout == "2d" else inp.u), delta=g(inp.delta), A=g(inp.A),
+                    B=g(inp.B), C=g(inp.C), D=g(inp.D), dt_bias=g(inp.dt_bias))
+        nbytes = ss2d_bytes(shape, shape.batch) if layout == "2d" else seq_bytes(shape, shape.batch)
+        n = max(2, -(-ROTATE_BYTES // nbytes))
+        need = vmb.vmb_scan_workspace_bytes(True, shape.batch, 4, shape.channels, shape.L,
+                                            shape.N, lay)
+        sets = [{k: (v.clone() if i else v) for k, v in base.items()} for i in range(n)]
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        for name, opt in opts.items():
+            if layout == "2d" and opt & vmb.VMB_MEAN_NO_BROADCAST:
+                continue
+            if layout == "2d":
+                yshape = tuple(inp.x.shape)
+            else:
+                yshape = tuple(inp.delta.shape)
+                if opt & vmb.VMB_MEAN_NO_BROADCAST:
+                    yshape = yshape[:2] + (1,) + yshape[3:]
+            ys = [torch.empty(yshape, device=dev) for _ in range(n)]
+
+            def call(i):
+                d = sets[i % n]
+                vmb.vmb_mean_scan_fwd_ex(d["u"], d["delta"], d["A"], d["B"], d["C"], d["D"],
+                                         d["dt_bias"], True, ys[i % n], opt, layout=lay,
+                                         workspace=ws, stream=stream)
+            for i in range(warmup):
+                call(i)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(steps):
+                call(i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            rows.append({"layout": layout, "reading": name, "options": opt,
+                         "us": round(e0.elapsed_time(e1) * 1e3 / steps, 3)})
+            del ys
+        del sets, ws
+        torch.cuda.empty_cache()
+    return {"metric": "VMeanba reading variants, stage-1 56x56 c192 N16 fp32 (us/call)",
+            "unit": "us/call", "dtype": "f32", "data": "synthetic", "rows": rows}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -360,6 +422,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calibrate", action="store_true",
                     help="run a 256 MiB copy first (counter calibration dispatch)")
+    ap.add_argument("--variants", action="store_true",
+                    help="after the main line, print a line timing the mean scan's reading "
+                         "variants (vmb_mean_scan_fwd_ex options) at the main workload")
     ap.add_argument("--table1", action="store_true",
                     help="after the main line, print a second JSON line: the one-state scan "
                          "on materialised inputs at the paper's Table 1 shapes")
@@ -421,6 +486,8 @@ def main():
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
     print(json.dumps(out), flush=True)
+    if args.variants:
+        print(json.dumps(variants_bench(args.steps, args.warmup)), flush=True)
     if args.table1:
         print(json.dumps(table1_bench(max(5, args.steps // 10), 3)), flush=True)
 

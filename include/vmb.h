@@ -159,6 +159,45 @@ vmb_status vmb_mean_scan_fwd(const void* u, const void* delta, const float* A, c
                              void* workspace, size_t workspace_bytes, vmb_stream_t stream);
 
 /*
+ * Other readings of where T acts in eq. 9 (Section 2.2), as bit flags for
+ * vmb_mean_scan_fwd_ex. The paper states T on (Abar, Bbar u, C) and leaves
+ * the skip term and the output shape open; these select the alternatives.
+ */
+typedef enum {
+    /* D u stays outside T, per channel as in eq. 3:
+     *   ytilde_t = sum_n C[b,k,n,t] h_t[n]   (no r_mean)
+     *   y[b,k,d,t] = ytilde_t + D[c] u[b,k,d,t]
+     * 2D layout: each channel adds ((D[0,d] + D[2,d]) + (D[1,d] + D[3,d])) x[b,d,h,w]
+     * to the merged reduced output. */
+    VMB_MEAN_SKIP_PER_CHANNEL = 1,
+    /* T averages the raw timescale, input and state matrix, and the scan
+     * discretises the means (eq. 4 after T):
+     *   Delta_mean[t] = mean_d Delta_{d,t}, u_mean[t] = mean_d u[b,k,d,t],
+     *   A_mean[n] = mean_d A[c,n],
+     *   h_t[n] = exp(Delta_mean[t] A_mean[n]) h_{t-1}[n] + Delta_mean[t] B[b,k,n,t] u_mean[t] */
+    VMB_MEAN_RAW = 2,
+    /* T^-1 left out: y is [batch, K, 1, L] and holds ytilde (SEQ layout only;
+     * not with VMB_MEAN_SKIP_PER_CHANNEL) */
+    VMB_MEAN_NO_BROADCAST = 4
+} vmb_mean_option;
+
+/*
+ * vmb_mean_scan_fwd with a reading of T chosen by `options` (a bitwise OR of
+ * vmb_mean_option values; 0 is vmb_mean_scan_fwd). Arguments and workspace as
+ * for vmb_mean_scan_fwd, except that y is [batch, K, 1, L] with
+ * VMB_MEAN_NO_BROADCAST. Errors as for vmb_mean_scan_fwd, plus
+ * VMB_ERR_UNSUPPORTED for an unknown bit, VMB_MEAN_NO_BROADCAST with the 2D
+ * layout, or VMB_MEAN_NO_BROADCAST with VMB_MEAN_SKIP_PER_CHANNEL.
+ */
+vmb_status vmb_mean_scan_fwd_ex(const void* u, const void* delta, const float* A, const void* B,
+                                const void* C, const float* D, const float* dt_bias,
+                                int delta_softplus, void* y, int64_t batch, int64_t K,
+                                int64_t channels, int64_t L, int64_t N, vmb_dtype in_dtype,
+                                vmb_dtype out_dtype, vmb_layout layout, int64_t H, int64_t W,
+                                void* workspace, size_t workspace_bytes, unsigned options,
+                                vmb_stream_t stream);
+
+/*
  * One-state scan on materialised, discretised inputs: the decomposition of
  * the paper's kernel experiments (Appendix D: the kernel only walks the
  * recurrence of eq. 3, discretisation runs outside it; Table 1 shapes, one

@@ -85,12 +85,46 @@ struct MeanWs {
     float* ytil;  // 2-D layout: reduced output ytilde[bk][t]
 };
 
+// How the reduced output leaves (sequence layout): skip_own adds each
+// channel's own D[c] u[d, t] to the broadcast value (which then holds no
+// r_mean); no_bcast stores one row per (batch, k) instead of broadcasting.
+struct StoreOpts {
+    int skip_own;
+    int no_bcast;
+};
+
+// Store ytilde at position t for the channels d0 + wv, d0 + wv + step, ...
+// below d1 of sequence bk (sequence layout).
+template <typename Tin, typename Tout>
+__device__ __forceinline__ void store_reduced(float yt, Tout* __restrict__ y,
+                                              const Tin* __restrict__ u,
+                                              const float* __restrict__ D, StoreOpts so,
+                                              size_t bk, int k, int Dc, int L, int t, int wv,
+                                              int step, int d0, int d1) {
+    if (so.no_bcast) {
+        if (wv == 0 && d0 == 0) y[bk * L + t] = from_f32<Tout>(yt);
+        return;
+    }
+    if (so.skip_own && D) {
+        for (int d = d0 + wv; d < d1; d += step) {
+            const size_t off = (bk * Dc + d) * static_cast<size_t>(L) + t;
+            y[off] = from_f32<Tout>(__builtin_fmaf(D[static_cast<size_t>(k) * Dc + d],
+                                                   to_f32(u[off]), yt));
+        }
+        return;
+    }
+    const Tout o = from_f32<Tout>(yt);
+    for (int d = d0 + wv; d < d1; d += step) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
+}
+
 // Reduce stage of one chunk (chunk blockIdx.x of sequence (blockIdx.z,
 // blockIdx.y)): every wave's partial sums over its channels, for the lanes'
 // positions, left in part[wv][0..N+2) (exp sums per state, s, r).
-template <int N, typename Tin, bool kTwoD>
+// A wave's partial sums fill N + 2 rows (exp sums per state, s, r), one more
+// (the input sum) when T averages the raw terms.
+template <int N, typename Tin, bool kTwoD, bool kRaw>
 __device__ __forceinline__ void reduce_partials(
-    float (*part)[N + 2][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
+    float (*part)[N + 2 + int(kRaw)][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
     const float* __restrict__ A, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, int K, int Dc, int L, int H, int W, int C, int softplus) {
     // Each wave's slice part[wv] first holds its channel parameters (two
@@ -119,7 +153,7 @@ __device__ __forceinline__ void reduce_partials(
     float acc[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) acc[n] = 0.0f;
-    float s = 0.0f, r = 0.0f;
+    float s = 0.0f, r = 0.0f, q = 0.0f;
     const int d0 = (wv * Dc) / kRedWaves, d1 = ((wv + 1) * Dc) / kRedWaves;
     const int nw = d1 - d0;  // channels of this wave
     float* prm = &part[wv][0][0];
@@ -173,15 +207,26 @@ __device__ __forceinline__ void reduce_partials(
     };
     auto channel = [&](const float (&an)[N], float bias, float dskip, float dv, float uv) {
         const float dl = valid ? timescale(dv + bias, sp) : 0.0f;
+        if constexpr (kRaw) {
+            // sums of A log2(e) (the same in every lane), Delta and u
 #pragma unroll
-        for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl * an[n]);  // an = A log2(e)
-        s = __builtin_fmaf(dl, uv, s);
+            for (int n = 0; n < N; ++n) acc[n] += an[n];
+            s += dl;
+            q += uv;
+        } else {
+#pragma unroll
+            for (int n = 0; n < N; ++n) acc[n] += fast_exp2(dl * an[n]);  // an = A log2(e)
+            s = __builtin_fmaf(dl, uv, s);
+        }
         r = __builtin_fmaf(dskip, uv, r);
         // the sums are formed here, not sunk towards their next use (which
         // would keep every channel's parameters live)
 #pragma unroll
         for (int n = 0; n < N; ++n) asm volatile("" : "+v"(acc[n]));
-        asm volatile("" : "+v"(s), "+v"(r));
+        if constexpr (kRaw)
+            asm volatile("" : "+v"(s), "+v"(r), "+v"(q));
+        else
+            asm volatile("" : "+v"(s), "+v"(r));
     };
 
     if (nw > 0) {
@@ -228,16 +273,43 @@ __device__ __forceinline__ void reduce_partials(
     for (int n = 0; n < N; ++n) part[wv][n][lane] = acc[n];
     part[wv][N][lane] = s;
     part[wv][N + 1][lane] = r;
+    if constexpr (kRaw) part[wv][N + 2][lane] = q;
 }
 
-template <int N, typename Tin, bool kTwoD>
+// The pair (a, b) of state n at one position from the channel-group sums:
+// the means of the discretised terms, (mean exp(Delta A), B mean(Delta u)),
+// or with kRaw the discretisation of the means, (exp(mean Delta mean A),
+// mean Delta B mean u).
+template <int N, bool kRaw>
+__device__ __forceinline__ void reduced_pair(const float (*part)[N + 2 + int(kRaw)][kC], int n,
+                                             int lane, float inv, float bval, float& a,
+                                             float& bb) {
+    float sm = 0.0f, am = 0.0f;
+    for (int w = 0; w < kRedWaves; ++w) sm += part[w][N][lane];
+    for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
+    sm *= inv;
+    am *= inv;
+    if constexpr (kRaw) {
+        float um = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) um += part[w][N + 2][lane];
+        um *= inv;
+        a = fast_exp2(sm * am);  // am = mean A log2(e)
+        bb = sm * bval * um;
+    } else {
+        a = am;
+        bb = bval * sm;
+    }
+}
+
+template <int N, typename Tin, bool kTwoD, bool kRaw>
 __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
     int softplus) {
-    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
-    reduce_partials<N, Tin, kTwoD>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C, softplus);
+    __shared__ __align__(16) float part[kRedWaves][N + 2 + int(kRaw)][kC];
+    reduce_partials<N, Tin, kTwoD, kRaw>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
+                                         softplus);
     __syncthreads();
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
@@ -250,9 +322,6 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     // channel groups added in a fixed order; wave w then scans states
     // w, w + 16, ... of this chunk
     const float inv = 1.0f / static_cast<float>(Dc);
-    float sm = 0.0f;
-    for (int w = 0; w < kRedWaves; ++w) sm += part[w][N][lane];
-    sm *= inv;
     if (wv == 0) {
         float rm = 0.0f;
         for (int w = 0; w < kRedWaves; ++w) rm += part[w][N + 1][lane];
@@ -261,12 +330,11 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     float* scan_bk = ws.scan + bk * N * L * 2;
     float* agg_bk = ws.agg + bk * N * nchunks * 2;
     for (int n = wv; n < N; n += kRedWaves) {
-        float am = 0.0f;
-        for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
-        am *= inv;
+        float a, bb;
+        reduced_pair<N, kRaw>(part, n, lane, inv, to_f32(Bm[(bk * N + n) * L + tc]), a, bb);
         // positions past the end act as the identity (1, 0)
-        float a = valid ? am : 1.0f;
-        float bb = valid ? to_f32(Bm[(bk * N + n) * L + tc]) * sm : 0.0f;
+        a = valid ? a : 1.0f;
+        bb = valid ? bb : 0.0f;
         wave_scan(a, bb);
         if (valid) {
             float2 v = make_float2(a, bb);
@@ -333,19 +401,19 @@ __device__ __forceinline__ void get_pair(float* p, float& a, float& b) {
     b = __uint_as_float(static_cast<unsigned>(v >> 32));
 }
 
-template <int N, typename Tin, typename Tout, bool kTwoD>
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw>
 __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
     const float* __restrict__ dt_bias, const Tin* __restrict__ xt, MeanWs ws,
     unsigned long long* __restrict__ flags, unsigned long long epoch, Tout* __restrict__ y, int K,
-    int Dc, int L, int H, int W, int nchunks, int softplus) {
+    int Dc, int L, int H, int W, int nchunks, int softplus, StoreOpts so) {
     static_assert(N <= kRedWaves, "one state per wave");
-    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
+    __shared__ __align__(16) float part[kRedWaves][N + 2 + int(kRaw)][kC];
     __shared__ float yst[kRedWaves][kC];  // C h of state n at each position
     __shared__ float rsh[kC];             // r_mean at each position
-    reduce_partials<N, Tin, kTwoD>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, kC,
-                                   softplus);
+    reduce_partials<N, Tin, kTwoD, kRaw>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, kC,
+                                         softplus);
     __syncthreads();
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
@@ -362,14 +430,10 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     if (wv < N) {
         const int n = wv;
         cv = valid ? to_f32(Cm[(bk * N + n) * L + tc]) : 0.0f;
-        float sm = 0.0f, am = 0.0f;
-        for (int w = 0; w < kRedWaves; ++w) sm += part[w][N][lane];
-        for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
-        sm *= inv;
-        am *= inv;
+        reduced_pair<N, kRaw>(part, n, lane, inv, to_f32(Bm[(bk * N + n) * L + tc]), a, bb);
         // positions past the end act as the identity (1, 0)
-        a = valid ? am : 1.0f;
-        bb = valid ? to_f32(Bm[(bk * N + n) * L + tc]) * sm : 0.0f;
+        a = valid ? a : 1.0f;
+        bb = valid ? bb : 0.0f;
         wave_scan(a, bb);
         if (lane == kC - 1) put_pair(agg_bk + (static_cast<size_t>(n) * nchunks + chunk) * 2, a, bb);
     } else if (wv == N) {
@@ -414,14 +478,13 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     }
     __syncthreads();
     if (!valid) return;
-    float yt = rsh[lane];
+    float yt = so.skip_own ? 0.0f : rsh[lane];
 #pragma unroll
     for (int n = 0; n < N; ++n) yt += yst[n][lane];
     if constexpr (kTwoD) {
         if (wv == 0) ws.ytil[bk * L + t] = yt;
     } else {
-        const Tout o = from_f32<Tout>(yt);
-        for (int d = wv; d < Dc; d += kRedWaves) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
+        store_reduced<Tin, Tout>(yt, y, u, D, so, bk, k, Dc, L, t, wv, kRedWaves, 0, Dc);
     }
 }
 
@@ -491,11 +554,10 @@ __device__ __forceinline__ void ch_partials(const MeanWs& ws, const Tin* __restr
 // With kTwoD the reduced sequence itself is stored (to ws.ytil) for the
 // merge-and-broadcast pass.
 template <int N, typename Tin, typename Tout, bool kTwoD>
-__global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(MeanWs ws,
-                                                                 const Tin* __restrict__ Cm,
-                                                                 Tout* __restrict__ y, int K,
-                                                                 int Dc, int L, int C, int nchunks,
-                                                                 int groups, int inline_carry) {
+__global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(
+    MeanWs ws, const Tin* __restrict__ Cm, Tout* __restrict__ y, const Tin* __restrict__ u,
+    const float* __restrict__ D, int K, int Dc, int L, int C, int nchunks, int groups,
+    int inline_carry, StoreOpts so) {
     __shared__ float part[kFinWaves][kC];
     const int blk = blockIdx.x, k = blockIdx.y / groups, grp = blockIdx.y % groups;
     const int b = blockIdx.z;
@@ -512,26 +574,29 @@ __global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(MeanWs ws,
     part[wv][lane] = acc[0];
     __syncthreads();
     if (!valid) return;
-    float yt = ws.rmean[bk * L + tc];
+    float yt = so.skip_own ? 0.0f : ws.rmean[bk * L + tc];
 #pragma unroll
     for (int w = 0; w < kFinWaves; ++w) yt += part[w][lane];
     if constexpr (kTwoD) {
         if (wv == 0) ws.ytil[bk * L + t] = yt;
         return;
     }
-    const Tout o = from_f32<Tout>(yt);
     const int dg0 = (grp * Dc) / groups, dg1 = ((grp + 1) * Dc) / groups;
-    for (int d = dg0 + wv; d < dg1; d += kFinWaves) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
+    store_reduced<Tin, Tout>(yt, y, u, D, so, bk, k, Dc, L, t, wv, kFinWaves, dg0, dg1);
 }
 
 // 2-D layout: fold the four reduced sequences of each batch element into one
 // map, (y0 + y2) + (y1 + y3) per pixel (the cross-merge, same association as
 // the standalone merge), and broadcast it to the channels of group blockIdx.y.
+// With a per-channel skip (x given) each channel adds the merge of its four
+// directions' D[k, d] x[b, d, pixel] terms, (D0 + D2) + (D1 + D3) times x.
 // grid: (block of 256 pixels, channel groups, batch).
-template <typename Tout>
+template <typename Tin, typename Tout>
 __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __restrict__ ytil,
-                                                              Tout* __restrict__ y, int Dc, int H,
-                                                              int W, int groups) {
+                                                              Tout* __restrict__ y,
+                                                              const Tin* __restrict__ x,
+                                                              const float* __restrict__ D, int Dc,
+                                                              int H, int W, int groups) {
     const int L = H * W;
     const int p = blockIdx.x * 256 + threadIdx.x;
     const int grp = blockIdx.y, b = blockIdx.z;
@@ -541,9 +606,19 @@ __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __res
     const float* yb = ytil + static_cast<size_t>(b) * 4 * L;
     const float s02 = yb[p] + yb[2 * static_cast<size_t>(L) + (L - 1 - p)];
     const float s13 = yb[static_cast<size_t>(L) + q] + yb[3 * static_cast<size_t>(L) + (L - 1 - q)];
-    const Tout o = from_f32<Tout>(s02 + s13);
+    const float ym = s02 + s13;
     const int dg0 = (grp * Dc) / groups, dg1 = ((grp + 1) * Dc) / groups;
     Tout* yp = y + static_cast<size_t>(b) * Dc * L + p;
+    if (x) {
+        const Tin* xp = x + static_cast<size_t>(b) * Dc * L + p;
+        for (int d = dg0; d < dg1; ++d) {
+            const float dsum = (D[d] + D[2 * Dc + d]) + (D[Dc + d] + D[3 * Dc + d]);
+            yp[static_cast<size_t>(d) * L] =
+                from_f32<Tout>(__builtin_fmaf(dsum, to_f32(xp[static_cast<size_t>(d) * L]), ym));
+        }
+        return;
+    }
+    const Tout o = from_f32<Tout>(ym);
     for (int d = dg0; d < dg1; ++d) yp[static_cast<size_t>(d) * L] = o;
 }
 
@@ -554,15 +629,18 @@ inline int clamp_groups(long long want, int Dc) {
     return static_cast<int>(want < 1 ? 1 : (want > most ? most : want));
 }
 
-template <typename Tout>
+template <typename Tin, typename Tout>
 vmb_status launch_merge_broadcast(const float* ytil, const ScanArgs& a) {
     const int Dc = int(a.channels), H = int(a.H), W = int(a.W), L = H * W;
     const int pblk = (L + 255) / 256;
     const long long mwant = (512 + pblk * a.batch - 1) / (pblk * a.batch);
     const int mgroups = clamp_groups(mwant, Dc);
-    hipLaunchKernelGGL(k_mean_merge_broadcast<Tout>,
+    // per-channel skip: x and D (an absent D makes it the reduced output alone)
+    const bool own = (a.options & VMB_MEAN_SKIP_PER_CHANNEL) && a.D;
+    hipLaunchKernelGGL((k_mean_merge_broadcast<Tin, Tout>),
                        dim3(pblk, static_cast<unsigned>(mgroups), unsigned(a.batch)), dim3(256), 0,
-                       a.stream, ytil, static_cast<Tout*>(a.y), Dc, H, W, mgroups);
+                       a.stream, ytil, static_cast<Tout*>(a.y),
+                       own ? static_cast<const Tin*>(a.u) : nullptr, a.D, Dc, H, W, mgroups);
     return check_launch();
 }
 
@@ -582,7 +660,7 @@ unsigned long long next_epoch() {
     return e ? e : counter.fetch_add(2, std::memory_order_relaxed);
 }
 
-template <int N, typename Tin, typename Tout, bool kTwoD>
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw>
 vmb_status run(const ScanArgs& a) {
     const size_t bkn = static_cast<size_t>(a.batch * a.K);
     const MeanWsLayout lay = mean_ws_layout(a.batch, a.K, a.channels, a.L, N, kTwoD);
@@ -613,18 +691,22 @@ vmb_status run(const ScanArgs& a) {
         if (s0 != VMB_OK) return s0;
         xt = reinterpret_cast<const Tin*>(p + lay.xt);
     }
+    StoreOpts so;
+    so.skip_own = (a.options & VMB_MEAN_SKIP_PER_CHANNEL) ? 1 : 0;
+    so.no_bcast = (a.options & VMB_MEAN_NO_BROADCAST) ? 1 : 0;
     if (fused) {
-        hipLaunchKernelGGL((k_mean_fused<N, Tin, Tout, kTwoD>), grid, dim3(kC * kRedWaves), 0,
-                           a.stream, static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta),
-                           a.A, static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D,
-                           a.dt_bias, xt, ws, reinterpret_cast<unsigned long long*>(p + lay.flags),
-                           next_epoch(), static_cast<Tout*>(a.y), K, Dc, L, H, W, nchunks,
-                           a.softplus);
+        hipLaunchKernelGGL((k_mean_fused<N, Tin, Tout, kTwoD, kRaw>), grid, dim3(kC * kRedWaves),
+                           0, a.stream, static_cast<const Tin*>(a.u),
+                           static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
+                           static_cast<const Tin*>(a.C), a.D, a.dt_bias, xt, ws,
+                           reinterpret_cast<unsigned long long*>(p + lay.flags), next_epoch(),
+                           static_cast<Tout*>(a.y), K, Dc, L, H, W, nchunks, a.softplus, so);
         const vmb_status sf = check_launch();
         if (sf != VMB_OK || !kTwoD) return sf;
-        return launch_merge_broadcast<Tout>(ws.ytil, a);
+        return launch_merge_broadcast<Tin, Tout>(ws.ytil, a);
     }
-    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD>), grid, dim3(kC * kRedWaves), 0, a.stream,
+    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD, kRaw>), grid, dim3(kC * kRedWaves), 0,
+                       a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), a.D, a.dt_bias, xt, ws, K, Dc, L, H, W, C,
                        nchunks, a.softplus);
@@ -644,26 +726,34 @@ vmb_status run(const ScanArgs& a) {
     const int nblk = (L + kC - 1) / kC;
     const long long seqs = a.batch * a.K;
     const long long want = (512 + nblk * seqs - 1) / (nblk * seqs);
-    const int groups = kTwoD ? 1 : clamp_groups(want, Dc);
+    const int groups = kTwoD || so.no_bcast ? 1 : clamp_groups(want, Dc);
     hipLaunchKernelGGL((k_mean_finish_seq<N, Tin, Tout, kTwoD>),
                        dim3(nblk, static_cast<unsigned>(a.K * groups), unsigned(a.batch)),
                        dim3(kC * kFinWaves), 0, a.stream, ws, static_cast<const Tin*>(a.C),
-                       static_cast<Tout*>(a.y), K, Dc, L, C, nchunks, groups, inline_carry);
+                       static_cast<Tout*>(a.y), static_cast<const Tin*>(a.u), a.D, K, Dc, L, C,
+                       nchunks, groups, inline_carry, so);
     st = check_launch();
     if (st != VMB_OK || !kTwoD) return st;
-    return launch_merge_broadcast<Tout>(ws.ytil, a);
+    return launch_merge_broadcast<Tin, Tout>(ws.ytil, a);
+}
+
+template <int N, typename Tin, typename Tout, bool kRaw>
+vmb_status dispatch_layout(const ScanArgs& a) {
+    return a.layout == VMB_LAYOUT_SEQ ? run<N, Tin, Tout, false, kRaw>(a)
+                                      : run<N, Tin, Tout, true, kRaw>(a);
 }
 
 template <int N, typename Tin, typename Tout>
-vmb_status dispatch_layout(const ScanArgs& a) {
-    return a.layout == VMB_LAYOUT_SEQ ? run<N, Tin, Tout, false>(a) : run<N, Tin, Tout, true>(a);
+vmb_status dispatch_reading(const ScanArgs& a) {
+    return (a.options & VMB_MEAN_RAW) ? dispatch_layout<N, Tin, Tout, true>(a)
+                                      : dispatch_layout<N, Tin, Tout, false>(a);
 }
 
 template <int N>
 vmb_status dispatch_dtype(const ScanArgs& a) {
-    if (a.in_dt == VMB_F32) return dispatch_layout<N, float, float>(a);
-    if (a.out_dt == VMB_BF16) return dispatch_layout<N, bf16_t, bf16_t>(a);
-    return dispatch_layout<N, bf16_t, float>(a);
+    if (a.in_dt == VMB_F32) return dispatch_reading<N, float, float>(a);
+    if (a.out_dt == VMB_BF16) return dispatch_reading<N, bf16_t, bf16_t>(a);
+    return dispatch_reading<N, bf16_t, float>(a);
 }
 
 }  // namespace

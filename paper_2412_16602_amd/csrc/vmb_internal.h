@@ -28,6 +28,7 @@ struct ScanArgs {
     int64_t H, W;
     void* ws;
     size_t ws_bytes;
+    unsigned options;  // vmb_mean_option bits (mean scan only)
     hipStream_t stream;
 };
 

@@ -121,6 +121,12 @@ vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
         if (a.K != 4 || a.H < 1 || a.W < 1 || prod({a.H, a.W}) != a.L) return VMB_ERR_SHAPE;
     }
     if (!supported_n(a.N)) return VMB_ERR_UNSUPPORTED;
+    const unsigned known = VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST;
+    if (a.options & ~known) return VMB_ERR_UNSUPPORTED;
+    if (a.options && !mean_variant) return VMB_ERR_UNSUPPORTED;
+    const bool no_bcast = (a.options & VMB_MEAN_NO_BROADCAST) != 0;
+    if (no_bcast && (a.layout != VMB_LAYOUT_SEQ || (a.options & VMB_MEAN_SKIP_PER_CHANNEL)))
+        return VMB_ERR_UNSUPPORTED;
     // the chunk-local index math of the mean variant's passes is 32-bit
     if (mean_variant && prod({a.batch, a.K, a.N + 2, a.L}) > kMaxRow) return VMB_ERR_UNSUPPORTED;
     const void* streamed[] = {a.u, a.delta, a.B, a.C, a.y};
@@ -138,7 +144,7 @@ vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
     // aliasing: the output must not overlap any input (or the workspace)
     const size_t ein = dsize(a.in_dt), eout = dsize(a.out_dt);
     const int64_t u_elems = a.layout == VMB_LAYOUT_2D ? seq / a.K : seq;
-    const int64_t y_elems = a.layout == VMB_LAYOUT_2D ? seq / a.K : seq;
+    const int64_t y_elems = a.layout == VMB_LAYOUT_2D ? seq / a.K : (no_bcast ? seq / a.channels : seq);
     const Range ry = range_of(a.y, y_elems, eout);
     const Range inputs[] = {range_of(a.u, u_elems, ein),
                             range_of(a.delta, seq, ein),

@@ -22,6 +22,8 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vmb.h")
 
 VMB_F32, VMB_BF16 = 0, 1
 VMB_LAYOUT_SEQ, VMB_LAYOUT_2D = 0, 1
+# vmb_mean_option bits (vmb_mean_scan_fwd_ex)
+VMB_MEAN_SKIP_PER_CHANNEL, VMB_MEAN_RAW, VMB_MEAN_NO_BROADCAST = 1, 2, 4
 
 STATUS = {0: "VMB_OK", 1: "VMB_ERR_NULL", 2: "VMB_ERR_SHAPE", 3: "VMB_ERR_DTYPE",
           4: "VMB_ERR_ALIGN", 5: "VMB_ERR_ALIAS", 6: "VMB_ERR_UNSUPPORTED",
@@ -57,6 +59,8 @@ def load_library():
         fn = getattr(lib, name)
         fn.argtypes = scan
         fn.restype = I
+    lib.vmb_mean_scan_fwd_ex.argtypes = scan[:-1] + [ctypes.c_uint, P]
+    lib.vmb_mean_scan_fwd_ex.restype = I
     lib.vmb_discrete_scan.argtypes = [P, P, P, P, P, I64, I64, I64, P]
     lib.vmb_discrete_scan.restype = I
     lib.vmb_channel_mean.argtypes = [P, P, I64, I64, I64, P]
@@ -166,7 +170,7 @@ def vmb_scan_workspace_bytes(mean_variant: bool, batch: int, K: int, channels: i
 
 
 def _scan(name, mean_variant, u, delta, A, B, C, D, dt_bias, delta_softplus, y, layout,
-          workspace, stream):
+          workspace, stream, options=None):
     lib = load_library()
     batch, K, channels, L = delta.shape
     N = A.shape[1]
@@ -179,17 +183,34 @@ def _scan(name, mean_variant, u, delta, A, B, C, D, dt_bias, delta_softplus, y, 
         if u.dim() != 4 or u.shape[0] != batch or u.shape[1] != channels:
             raise ValueError("2-D layout: u must be x [batch, channels, H, W]")
         H, W = int(u.shape[2]), int(u.shape[3])
+        y_shape = (batch, channels, H, W)
     else:
         H, W = 1, L
+        if tuple(u.shape) != (batch, K, channels, L):
+            raise ValueError(f"u shape {tuple(u.shape)} != {(batch, K, channels, L)}")
+        rows = 1 if options and options & VMB_MEAN_NO_BROADCAST else channels
+        y_shape = (batch, K, rows, L)
+    if tuple(y.shape) != y_shape:
+        raise ValueError(f"y shape {tuple(y.shape)} != {y_shape}")
+    for t, nm in ((B, "B"), (C, "C")):
+        if tuple(t.shape) != (batch, K, N, L):
+            raise ValueError(f"{nm} shape {tuple(t.shape)} != {(batch, K, N, L)}")
+    if tuple(A.shape) != (K * channels, N):
+        raise ValueError(f"A shape {tuple(A.shape)} != {(K * channels, N)}")
+    for t, nm in ((D, "D"), (dt_bias, "dt_bias")):
+        if t is not None and t.numel() != K * channels:
+            raise ValueError(f"{nm} must hold K * channels = {K * channels} values")
     if workspace is None:
         need = vmb_scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout)
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=delta.device) if need else None
     ws_ptr = _dev(workspace, "workspace")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    status = getattr(lib, name)(
-        _dev(u, "u"), _dev(delta, "delta"), _f32(A, "A"), _dev(B, "B"), _dev(C, "C"),
-        _f32(D, "D"), _f32(dt_bias, "dt_bias"), int(bool(delta_softplus)), _dev(y, "y"),
-        batch, K, channels, L, N, in_dt, out_dt, layout, H, W, ws_ptr, ws_bytes, _stream(stream))
+    args = [_dev(u, "u"), _dev(delta, "delta"), _f32(A, "A"), _dev(B, "B"), _dev(C, "C"),
+            _f32(D, "D"), _f32(dt_bias, "dt_bias"), int(bool(delta_softplus)), _dev(y, "y"),
+            batch, K, channels, L, N, in_dt, out_dt, layout, H, W, ws_ptr, ws_bytes]
+    if options is not None:
+        args.append(int(options))
+    status = getattr(lib, name)(*args, _stream(stream))
     _check(status, name)
     return y
 
@@ -206,6 +227,14 @@ def vmb_mean_scan_fwd(u, delta, A, B, C, D, dt_bias, delta_softplus, y,
     """VMeanba channel-mean scan; shapes as in include/vmb.h. Returns y."""
     return _scan("vmb_mean_scan_fwd", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
                  y, layout, workspace, stream)
+
+
+def vmb_mean_scan_fwd_ex(u, delta, A, B, C, D, dt_bias, delta_softplus, y, options: int,
+                         layout: int = VMB_LAYOUT_SEQ, workspace=None, stream=None):
+    """VMeanba scan with a reading of T chosen by ``options`` (VMB_MEAN_* bits;
+    y is [batch, K, 1, L] with VMB_MEAN_NO_BROADCAST). Returns y."""
+    return _scan("vmb_mean_scan_fwd_ex", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
+                 y, layout, workspace, stream, options=options)
 
 
 def vmb_discrete_scan(abar: torch.Tensor, bu: torch.Tensor, C: torch.Tensor,

@@ -65,8 +65,9 @@ def assert_close(got, ref, rtol, atol, what="", scale=None):
 
 
 def run_scan(inp: workloads.Inputs, variant: str, layout: str, out_dtype=None, softplus=True,
-             use_bias=True, use_d=True, delta=None, workspace=None):
-    """One call of vmb_selective_scan_fwd / vmb_mean_scan_fwd on cuda:0."""
+             use_bias=True, use_d=True, delta=None, workspace=None, options=None):
+    """One call of vmb_selective_scan_fwd / vmb_mean_scan_fwd on cuda:0
+    (vmb_mean_scan_fwd_ex when ``options`` is given)."""
     s = inp.shape
     lay = vmb.VMB_LAYOUT_2D if layout == "2d" else vmb.VMB_LAYOUT_SEQ
     u = upload_stream(inp, "x" if layout == "2d" else "u")
@@ -82,18 +83,28 @@ def run_scan(inp: workloads.Inputs, variant: str, layout: str, out_dtype=None, s
         out_dtype = torch.bfloat16 if s.dtype == "bf16" else torch.float32
     b = inp.delta.shape[0]
     shape = (b, s.channels, s.H, s.W) if layout == "2d" else tuple(inp.delta.shape)
+    if options is not None and options & vmb.VMB_MEAN_NO_BROADCAST and layout == "seq":
+        shape = shape[:2] + (1,) + shape[3:]
     y = torch.empty(shape, dtype=out_dtype, device=dev())
-    fn = vmb.vmb_selective_scan_fwd if variant == "full" else vmb.vmb_mean_scan_fwd
-    fn(u, dl, A, B, C, D, bias, softplus, y, layout=lay, workspace=workspace)
+    if options is not None:
+        assert variant == "mean"
+        vmb.vmb_mean_scan_fwd_ex(u, dl, A, B, C, D, bias, softplus, y, options, layout=lay,
+                                 workspace=workspace)
+    else:
+        fn = vmb.vmb_selective_scan_fwd if variant == "full" else vmb.vmb_mean_scan_fwd
+        fn(u, dl, A, B, C, D, bias, softplus, y, layout=lay, workspace=workspace)
     torch.cuda.synchronize()
     return y
 
 
 def oracle_seq(inp: workloads.Inputs, variant: str, layout: str, softplus=True, use_bias=True,
-               use_d=True, delta=None, sel=None):
-    """fp64 oracle on the same inputs (per-direction sequence outputs)."""
+               use_d=True, delta=None, sel=None, options=0):
+    """fp64 oracle on the same inputs (per-direction sequence outputs);
+    ``options`` are the oracle's mean-scan reading bits."""
     u = oracle.cross_scan(inp.x) if layout == "2d" else inp.u
     dl = inp.delta if delta is None else delta
-    fn = oracle.full_scan if variant == "full" else oracle.mean_scan
-    return fn(u, dl, inp.A, inp.B, inp.C, inp.D if use_d else None,
-              inp.dt_bias if use_bias else None, softplus, sel=sel)
+    args = (u, dl, inp.A, inp.B, inp.C, inp.D if use_d else None,
+            inp.dt_bias if use_bias else None, softplus)
+    if variant == "full":
+        return oracle.full_scan(*args, sel=sel)
+    return oracle.mean_scan(*args, sel=sel, options=options)

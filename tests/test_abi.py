@@ -26,7 +26,8 @@ def test_exports_every_declared_symbol(lib):
     names = vmb.declared_symbols()
     assert set(names) >= {"vmb_cross_scan", "vmb_cross_merge", "vmb_selective_scan_fwd",
                           "vmb_mean_scan_fwd", "vmb_scan_workspace_bytes", "vmb_status_string",
-                          "vmb_abi_version", "vmb_discrete_scan", "vmb_channel_mean"}
+                          "vmb_abi_version", "vmb_discrete_scan", "vmb_channel_mean",
+                          "vmb_mean_scan_fwd_ex"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -52,13 +53,16 @@ def scan_call(lib, fn="vmb_selective_scan_fwd", **kw):
              batch=1, K=4, channels=8, L=12, N=4, in_dt=F32, out_dt=F32, layout=SEQ, H=3, W=4,
              ws=P(8), ws_bytes=1 << 30, stream=None)
     a.update(kw)
-    return getattr(lib, fn)(a["u"], a["delta"], a["A"], a["B"], a["C"], a["D"], a["dt_bias"],
-                            a["sp"], a["y"], a["batch"], a["K"], a["channels"], a["L"], a["N"],
-                            a["in_dt"], a["out_dt"], a["layout"], a["H"], a["W"], a["ws"],
-                            a["ws_bytes"], a["stream"])
+    args = [a["u"], a["delta"], a["A"], a["B"], a["C"], a["D"], a["dt_bias"], a["sp"], a["y"],
+            a["batch"], a["K"], a["channels"], a["L"], a["N"], a["in_dt"], a["out_dt"],
+            a["layout"], a["H"], a["W"], a["ws"], a["ws_bytes"]]
+    if fn == "vmb_mean_scan_fwd_ex":
+        args.append(a.get("options", 0))
+    return getattr(lib, fn)(*args, a["stream"])
 
 
-@pytest.mark.parametrize("fn", ["vmb_selective_scan_fwd", "vmb_mean_scan_fwd"])
+@pytest.mark.parametrize("fn", ["vmb_selective_scan_fwd", "vmb_mean_scan_fwd",
+                                "vmb_mean_scan_fwd_ex"])
 @pytest.mark.parametrize("kw,expect", [
     (dict(u=None), NULL), (dict(delta=None), NULL), (dict(A=None), NULL), (dict(B=None), NULL),
     (dict(C=None), NULL), (dict(y=None), NULL),
@@ -73,6 +77,31 @@ def scan_call(lib, fn="vmb_selective_scan_fwd", **kw):
 ])
 def test_scan_rejects(lib, fn, kw, expect):
     assert scan_call(lib, fn, **kw) == expect
+
+
+def test_mean_options_rules(lib):
+    ex = "vmb_mean_scan_fwd_ex"
+    SKIP1, RAW, NOBC = vmb.VMB_MEAN_SKIP_PER_CHANNEL, vmb.VMB_MEAN_RAW, vmb.VMB_MEAN_NO_BROADCAST
+    # the descriptions of include/vmb.h carry the same values
+    with open(vmb.HEADER_PATH) as f:
+        text = f.read()
+    for name, val in (("VMB_MEAN_SKIP_PER_CHANNEL", SKIP1), ("VMB_MEAN_RAW", RAW),
+                      ("VMB_MEAN_NO_BROADCAST", NOBC)):
+        assert f"{name} = {val}" in text
+    # a call that passes validation reaches the launch, which fails on a host
+    # without a GPU (VMB_ERR_HIP): the status says validation let it through
+    passed = (OK, 8)
+    for opt in (0, SKIP1, RAW, NOBC, SKIP1 | RAW, RAW | NOBC):
+        assert scan_call(lib, ex, options=opt) in passed
+    assert scan_call(lib, ex, options=8) == UNSUP
+    assert scan_call(lib, ex, options=NOBC | SKIP1) == UNSUP
+    assert scan_call(lib, ex, options=NOBC, layout=TWO_D) == UNSUP
+    assert scan_call(lib, ex, options=SKIP1 | RAW, layout=TWO_D) in passed
+    # without the broadcast y holds batch*K*L elements: [P(7), +4*12*4 B) overlaps
+    # nothing here, and y placed just past the end of u (4*8*12 floats) is fine
+    assert scan_call(lib, ex, options=NOBC, y=P(0, 4 * 8 * 12 * 4)) in passed
+    assert scan_call(lib, ex, options=0, y=P(0, 4 * 8 * 12 * 4)) in passed
+    assert scan_call(lib, ex, options=NOBC, y=P(0, 4 * 8 * 12 * 4 - 16)) == ALIAS
 
 
 def test_workspace_rules(lib):
