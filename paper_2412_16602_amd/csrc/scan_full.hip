@@ -102,8 +102,9 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L > kShortMaxL; }
 
 vmb_status launch_full_scan(const ScanArgs& a) {
-    if (use_chunked_full(a) || use_short_full(a)) {
+    if (use_tiles_full(a) || use_chunked_full(a) || use_short_full(a)) {
         auto run = [&](void* y_seq) {
+            if (use_tiles_full(a)) return launch_full_tiles(a, y_seq);
             return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq);
         };
         if (a.layout == VMB_LAYOUT_SEQ) return run(a.y);

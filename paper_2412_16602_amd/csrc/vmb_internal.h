@@ -116,6 +116,12 @@ bool use_short_full(const ScanArgs& a);
 vmb_status launch_full_short(const ScanArgs& a, void* y_seq);
 // Whether the positions-over-lanes kernel is the better fit for this shape.
 bool use_chunked_full(const ScanArgs& a);
+// Channels over lanes, states over the four waves of a workgroup, positions
+// in tiles (N == 16, at least kTilesMinRows batch * K * channels rows);
+// writes sequence-layout output to y_seq.
+constexpr int64_t kTilesMinRows = 16384;
+bool use_tiles_full(const ScanArgs& a);
+vmb_status launch_full_tiles(const ScanArgs& a, void* y_seq);
 vmb_status launch_mean_scan(const ScanArgs& a);
 
 inline vmb_status check_launch() {
