@@ -402,6 +402,98 @@ def variants_bench(steps: int, warmup: int):
             "unit": "us/call", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 
+def workloads_bench(steps: int, warmup: int):
+    """Full and mean scans at every N = 16 workload (the stage-1 map, the
+    batch-32 later stages, batch-128 bf16, the high-resolution map), both
+    layouts: us per call with HIP events on the launch stream. Inputs are
+    drawn on the GPU with the distributions of workloads.make_inputs
+    (channel-shared base plus 0.05 noise, delta ~ N(0, 0.5), softplus(dt_bias)
+    log-uniform on [1e-3, 1e-1], B, C ~ N(0, 1), A = -(n + 1), D = 1; bf16
+    workloads round the streamed tensors), because the host generator takes
+    minutes at the batch-128 size; enough input sets are used in turn that
+    every call reads from HBM rather than the 256 MB MALL."""
+    import torch
+
+    from paper_2412_16602_amd import vmb
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device=dev)
+    g.manual_seed(2)
+    rows = []
+    for shp in (workloads.STAGE1, workloads.STAGE2, workloads.STAGE3, workloads.STAGE4,
+                workloads.BATCHED_BF16, workloads.HIRES):
+        b, K, Dc, L, N, H, W = shp.batch, 4, shp.channels, shp.L, shp.N, shp.H, shp.W
+        bf16 = shp.dtype == "bf16"
+        dt = torch.bfloat16 if bf16 else torch.float32
+        esz = 2 if bf16 else 4
+        A = -torch.arange(1, N + 1, device=dev, dtype=torch.float32).repeat(K * Dc, 1)
+        D = torch.ones(K * Dc, device=dev)
+        lo, hi = math.log(1e-3), math.log(1e-1)
+        dtv = torch.exp(torch.empty(K * Dc, device=dev).uniform_(lo, hi, generator=g))
+        dt_bias = torch.log(torch.expm1(dtv))
+        for layout in ("seq", "2d"):
+            lay = vmb.VMB_LAYOUT_2D if layout == "2d" else vmb.VMB_LAYOUT_SEQ
+            nbytes = ss2d_bytes(shp, b, esz, esz) if layout == "2d" else seq_bytes(shp, b, esz, esz)
+            n_sets = max(1, min(8, -(-ROTATE_BYTES // nbytes)))
+
+            def draw():
+                if layout == "2d":
+                    u = torch.randn(b, 1, H, W, device=dev, generator=g) + \
+                        0.05 * torch.randn(b, Dc, H, W, device=dev, generator=g)
+                else:
+                    u = torch.randn(b, K, 1, L, device=dev, generator=g) + \
+                        0.05 * torch.randn(b, K, Dc, L, device=dev, generator=g)
+                delta = math.sqrt(0.5) * torch.randn(b, K, Dc, L, device=dev, generator=g)
+                Bm = torch.randn(b, K, N, L, device=dev, generator=g)
+                Cm = torch.randn(b, K, N, L, device=dev, generator=g)
+                return [t.to(dt).contiguous() for t in (u, delta, Bm, Cm)]
+
+            sets = [draw() for _ in range(n_sets)]
+            yshape = (b, Dc, H, W) if layout == "2d" else (b, K, Dc, L)
+            y = torch.empty(yshape, device=dev, dtype=dt)
+            for variant in ("full", "mean"):
+                fn = vmb.vmb_selective_scan_fwd if variant == "full" else vmb.vmb_mean_scan_fwd
+                need = vmb.vmb_scan_workspace_bytes(variant == "mean", b, K, Dc, L, N, lay)
+                ws = torch.empty(need, dtype=torch.uint8, device=dev) if need else None
+
+                def call(i):
+                    u, delta, Bm, Cm = sets[i % n_sets]
+                    fn(u, delta, A, Bm, Cm, D, dt_bias, True, y, layout=lay, workspace=ws,
+                       stream=stream)
+                # about 0.2 s of calls per measurement
+                for i in range(warmup):
+                    call(i)
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                call(0)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                n = max(3, min(steps, int(0.2e6 / max(1.0, e0.elapsed_time(e1) * 1e3))))
+                e0.record(stream)
+                for i in range(n):
+                    call(i)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                us = e0.elapsed_time(e1) * 1e3 / n
+                elems = b * K * Dc * N * L
+                rows.append({"workload": shp.name, "layout": layout, "variant": variant,
+                             "dtype": shp.dtype, "us": round(us, 2), "calls": n,
+                             "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                             "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                             "alu_frac": round(elems * FLOP_PER_ELEM / (us * 1e-6) / 1e12
+                                               / ALU_PEAK_TFLOPS, 4) if variant == "full" else None})
+                del ws
+            del sets, y
+            torch.cuda.empty_cache()
+    return {"metric": "full and mean SS2D scans at every N=16 workload (us/call)",
+            "unit": "us/call", "data": "synthetic",
+            "timing": "HIP events on the launch stream around consecutive calls",
+            "rows": rows}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -425,6 +517,9 @@ def main():
     ap.add_argument("--variants", action="store_true",
                     help="after the main line, print a line timing the mean scan's reading "
                          "variants (vmb_mean_scan_fwd_ex options) at the main workload")
+    ap.add_argument("--workloads", action="store_true",
+                    help="after the main line, print a line timing the full and mean scans "
+                         "at every N=16 workload, both layouts")
     ap.add_argument("--table1", action="store_true",
                     help="after the main line, print a second JSON line: the one-state scan "
                          "on materialised inputs at the paper's Table 1 shapes")
@@ -488,6 +583,8 @@ def main():
     print(json.dumps(out), flush=True)
     if args.variants:
         print(json.dumps(variants_bench(args.steps, args.warmup)), flush=True)
+    if args.workloads:
+        print(json.dumps(workloads_bench(args.steps, 3)), flush=True)
     if args.table1:
         print(json.dumps(table1_bench(max(5, args.steps // 10), 3)), flush=True)
 

@@ -103,12 +103,22 @@ bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L > kShortMaxL;
 
 vmb_status launch_full_scan(const ScanArgs& a) {
     if (use_tiles_full(a) || use_chunked_full(a) || use_short_full(a)) {
-        auto run = [&](void* y_seq) {
-            if (use_tiles_full(a)) return launch_full_tiles(a, y_seq);
+        auto run = [&](void* y_seq, const void* xt) {
+            if (use_tiles_full(a)) return launch_full_tiles(a, y_seq, xt);
             return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq);
         };
-        if (a.layout == VMB_LAYOUT_SEQ) return run(a.y);
-        vmb_status st = run(a.ws);
+        if (a.layout == VMB_LAYOUT_SEQ) return run(a.y, nullptr);
+        // 2-D: the tile path reads directions 1 and 3 from column-major plane
+        // copies in the workspace
+        const void* xt = nullptr;
+        if (use_tiles_full(a) && full_ws_has_xt(a.batch, a.K, a.channels, a.L, a.N)) {
+            void* xtw = static_cast<char*>(a.ws) + full_ws_xt_offset(a.batch, a.K, a.channels, a.L);
+            vmb_status st = launch_transpose_planes(a.u, xtw, a.batch, a.channels, a.H, a.W,
+                                                    a.in_dt, a.stream);
+            if (st != VMB_OK) return st;
+            xt = xtw;
+        }
+        vmb_status st = run(a.ws, xt);
         if (st != VMB_OK) return st;
         return launch_cross_merge(a.ws, a.y, a.batch, a.channels, a.H, a.W, VMB_F32, a.out_dt,
                                   a.stream);

@@ -109,8 +109,8 @@ template <typename Tin, typename Tout, bool kTwoD>
 __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
-    const float* __restrict__ dt_bias, Tout* __restrict__ y, int K, int Dc, int L, int H, int W,
-    int softplus, int n_cg, int n_wg) {
+    const float* __restrict__ dt_bias, Tout* __restrict__ y, const Tin* __restrict__ xt, int K,
+    int Dc, int L, int H, int W, int softplus, int n_cg, int n_wg) {
     constexpr int N = 16;
     __shared__ float s_dl2[kWave][kStride];               // Delta * log2 e
     __shared__ float s_du[kWave][kStride];                // Delta * u
@@ -142,6 +142,11 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     const size_t ld_row = (static_cast<size_t>(bk) * Dc + ld_d) * static_cast<size_t>(L);
     const Tin* drow = delta + ld_row;
     const Tin* urow = kTwoD ? u + (static_cast<size_t>(b) * Dc + ld_d) * L : u + ld_row;
+    // 2-D layout: direction k's sequence is the plane read row-major (k even)
+    // or column-major (k odd: the transposed copy xt when given), forwards
+    // for k < 2 and backwards for k >= 2
+    const Tin* srow = (kTwoD && (k & 1) && xt) ? xt + (static_cast<size_t>(b) * Dc + ld_d) * L : urow;
+    const bool gather = kTwoD && (k & 1) && !xt;
     Tout* yrow = y + ld_row;
     // every row starts on a 4-element boundary: 4-element pieces are 16-byte
     // (fp32) or 8-byte (bf16) aligned vectors
@@ -172,8 +177,17 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
         const int t = tile_start(tile) + 4 * lq;
         load4(drow + t, dv, in_aligned, 4);
         if constexpr (kTwoD) {
+            if (gather) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) uv[e] = to_f32(urow[pixel_of(k, t + e, H, W)]);
+                for (int e = 0; e < 4; ++e) uv[e] = to_f32(urow[pixel_of(k, t + e, H, W)]);
+            } else if (k < 2) {
+                load4(srow + t, uv, in_aligned, 4);
+            } else {
+                float r[4];
+                load4(srow + (L - 4 - t), r, in_aligned, 4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) uv[e] = r[3 - e];
+            }
         } else {
             load4(urow + t, uv, in_aligned, 4);
         }
@@ -267,14 +281,15 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
 }
 
 template <typename Tin, typename Tout, bool kTwoD>
-vmb_status launch_tiles_impl(const ScanArgs& a, Tout* y) {
+vmb_status launch_tiles_impl(const ScanArgs& a, Tout* y, const void* xt) {
     const int n_cg = int((a.channels + kWave - 1) / kWave);
     const long long n_wg = static_cast<long long>(n_cg) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
     hipLaunchKernelGGL((k_full_scan_tiles<Tin, Tout, kTwoD>), dim3(static_cast<unsigned>(n_wg)),
                        dim3(kTileThreads), 0, a.stream, static_cast<const Tin*>(a.u),
                        static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
-                       static_cast<const Tin*>(a.C), a.D, a.dt_bias, y, int(a.K), int(a.channels),
+                       static_cast<const Tin*>(a.C), a.D, a.dt_bias, y, static_cast<const Tin*>(xt),
+                       int(a.K), int(a.channels),
                        int(a.L), int(a.H), int(a.W), a.softplus, n_cg, int(n_wg));
     return check_launch();
 }
@@ -292,15 +307,15 @@ bool use_tiles_full(const ScanArgs& a) {
     return rows >= kTilesMinRows;
 }
 
-vmb_status launch_full_tiles(const ScanArgs& a, void* y_seq) {
+vmb_status launch_full_tiles(const ScanArgs& a, void* y_seq, const void* xt) {
     const bool two_d = a.layout == VMB_LAYOUT_2D;
     if (a.in_dt == VMB_F32)
-        return two_d ? launch_tiles_impl<float, float, true>(a, static_cast<float*>(y_seq))
-                     : launch_tiles_impl<float, float, false>(a, static_cast<float*>(y_seq));
-    if (two_d) return launch_tiles_impl<bf16_t, float, true>(a, static_cast<float*>(y_seq));
+        return two_d ? launch_tiles_impl<float, float, true>(a, static_cast<float*>(y_seq), xt)
+                     : launch_tiles_impl<float, float, false>(a, static_cast<float*>(y_seq), xt);
+    if (two_d) return launch_tiles_impl<bf16_t, float, true>(a, static_cast<float*>(y_seq), xt);
     if (a.out_dt == VMB_BF16)
-        return launch_tiles_impl<bf16_t, bf16_t, false>(a, static_cast<bf16_t*>(y_seq));
-    return launch_tiles_impl<bf16_t, float, false>(a, static_cast<float*>(y_seq));
+        return launch_tiles_impl<bf16_t, bf16_t, false>(a, static_cast<bf16_t*>(y_seq), xt);
+    return launch_tiles_impl<bf16_t, float, false>(a, static_cast<float*>(y_seq), xt);
 }
 
 }  // namespace vmb

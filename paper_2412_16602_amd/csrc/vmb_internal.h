@@ -63,6 +63,7 @@ inline int mean_chunk(int64_t /*batch*/, int64_t /*K*/, int64_t /*L*/) { return 
 //   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL only,
 //                               column-major copies of the input planes
 constexpr int64_t kMeanTransposeMaxL = 6144;  // then H * (W + 1) <= 2 L fits LDS
+static_assert(kMeanTransposeMaxL == 6144, "full_ws_has_xt uses the same bound");
 struct MeanWsLayout {
     size_t scan, rmean, agg, carry, ytil, xt, flags, total;
 };
@@ -121,7 +122,26 @@ bool use_chunked_full(const ScanArgs& a);
 // writes sequence-layout output to y_seq.
 constexpr int64_t kTilesMinRows = 16384;
 bool use_tiles_full(const ScanArgs& a);
-vmb_status launch_full_tiles(const ScanArgs& a, void* y_seq);
+// The 2-D layout of that path also reads column-major copies of the input
+// planes (xt, written by launch_transpose_planes into the workspace after the
+// per-direction outputs), so directions 1 and 3 load contiguous rows.
+vmb_status launch_full_tiles(const ScanArgs& a, void* y_seq, const void* xt);
+// Full scan, 2-D layout: whether the workspace holds xt (the tile path's
+// shapes with planes the transpose kernel takes: L <= kMeanTransposeMaxL, so
+// H * (W + 1) <= 2 L; below 128 positions a plane spans a few cache lines and
+// the column-major reads gather it from L1 faster than a copy pass), where it
+// starts (after the per-direction fp32 outputs), and its size (4 bytes per
+// element, either input type).
+inline bool full_ws_has_xt(int64_t batch, int64_t K, int64_t channels, int64_t L, int64_t N) {
+    return N == 16 && L >= 128 && L <= 6144 && batch * K * channels >= kTilesMinRows;
+}
+inline size_t full_ws_xt_offset(int64_t batch, int64_t K, int64_t channels, int64_t L) {
+    const size_t seq = static_cast<size_t>(batch) * K * channels * L;
+    return (seq * 4 + 255) & ~size_t{255};
+}
+inline size_t full_ws_xt_bytes(int64_t batch, int64_t channels, int64_t L) {
+    return (static_cast<size_t>(batch) * channels * L * 4 + 255) & ~size_t{255};
+}
 vmb_status launch_mean_scan(const ScanArgs& a);
 
 inline vmb_status check_launch() {

@@ -98,8 +98,12 @@ size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t 
     if (seq < 0) return SIZE_MAX;
     auto round_up = [](size_t v) { return (v + 255) & ~size_t{255}; };
     if (!mean_variant) {
-        // 2-D layout: per-direction fp32 outputs, folded by the merge pass
-        return layout == VMB_LAYOUT_2D ? round_up(static_cast<size_t>(seq) * 4) : 0;
+        // 2-D layout: per-direction fp32 outputs, folded by the merge pass,
+        // then (tile path) column-major copies of the input planes
+        if (layout != VMB_LAYOUT_2D) return 0;
+        size_t bytes = round_up(static_cast<size_t>(seq) * 4);
+        if (full_ws_has_xt(batch, K, channels, L, N)) bytes += full_ws_xt_bytes(batch, channels, L);
+        return bytes;
     }
     return mean_ws_layout(batch, K, channels, L, N, layout == VMB_LAYOUT_2D).total;
 }

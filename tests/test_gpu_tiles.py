@@ -108,3 +108,24 @@ def test_deterministic():
     a = run_scan(inp, "full", "seq")
     b = run_scan(inp, "full", "seq")
     assert torch.equal(a, b)
+
+
+def test_2d_long_gather():
+    """L > 6144: the 2-D tile path reads directions 1 and 3 straight from the
+    plane (no column-major copy); sampled channels against the oracle."""
+    import oracle
+
+    H, W, Dc = 80, 80, 4096  # L 6400, 16384 rows
+    log(f"tiles full 2d gather {H}x{W} channels={Dc}")
+    inp = inputs(1, H, W, Dc, layout="2d", seed=9)
+    got = to_f64(run_scan(inp, "full", "2d"))
+    ds = [0, 1, 63, 64, 2047, 4095]
+    u = oracle.cross_scan(inp.x)
+    rows = [k * Dc + d for k in range(4) for d in ds]
+    seq = oracle.full_scan(u, inp.delta, inp.A, inp.B, inp.C, inp.D, inp.dt_bias, True,
+                           sel=rows).reshape(1, 4, len(ds), H * W)
+    seq = np.ascontiguousarray(seq)
+    ref = oracle.cross_merge(seq, H, W, "f64")
+    scale = oracle.cross_merge(np.abs(seq), H, W, "f64")
+    assert_close(got[:, ds], ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
+                 what="2d gather")
