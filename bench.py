@@ -54,7 +54,7 @@ ALU_PEAK_TFLOPS = VALU_SLOTS_PER_S * FLOP_PER_ELEM / SLOTS_PER_ELEM / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "full_scan_seq_56x56_c192_n16_traffic.txt")
 # the sources the profiled kernel is compiled from
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2412_16602_amd", "csrc", f)
-                  for f in ("scan_chunked.hip", "vmb_internal.h")]
+                  for f in ("scan_chunked.hip", "vmb_device.h")]
 METRIC = ("SS2D selective-scan µs/call + HBM GB/s (% peak), full vs mean, "
           "VMamba-T 56×56")
 ROTATE_BYTES = 768 << 20  # > 2x the 256 MB MALL

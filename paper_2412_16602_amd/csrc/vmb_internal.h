@@ -148,71 +148,6 @@ inline vmb_status check_launch() {
     return hipGetLastError() == hipSuccess ? VMB_OK : VMB_ERR_HIP;
 }
 
-// ---------------------------------------------------------------- device side
-
-constexpr float kLog2e = 1.4426950408889634f;
-
-struct bf16_t {
-    uint16_t bits;
-};
-
-__device__ __forceinline__ float to_f32(float v) { return v; }
-__device__ __forceinline__ float to_f32(bf16_t v) {
-    return __uint_as_float(static_cast<uint32_t>(v.bits) << 16);
-}
-
-template <typename T>
-__device__ __forceinline__ T from_f32(float v);
-template <>
-__device__ __forceinline__ float from_f32<float>(float v) { return v; }
-template <>
-__device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
-    // gfx950 converts with round-to-nearest-even in hardware (v_cvt_pk_bf16_f32).
-    __bf16 h = static_cast<__bf16>(v);
-    bf16_t r;
-    __builtin_memcpy(&r.bits, &h, 2);
-    return r;
-}
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
-
-// log(1 + e) for e in [0, 1], from log(1 + e) = 2 atanh(s), s = e / (2 + e)
-// in [0, 1/3], with the Maclaurin series of atanh truncated after s^15
-// (next term below 2e-9 relative). Branch-free and accurate for tiny e,
-// where log(1 + e) evaluated directly would lose the low bits of e.
-__device__ __forceinline__ float log1p_unit(float e) {
-    const float s = e * fast_rcp(2.0f + e);
-    const float s2 = s * s;
-    float p = 2.0f / 15.0f;
-    p = __builtin_fmaf(p, s2, 2.0f / 13.0f);
-    p = __builtin_fmaf(p, s2, 2.0f / 11.0f);
-    p = __builtin_fmaf(p, s2, 2.0f / 9.0f);
-    p = __builtin_fmaf(p, s2, 2.0f / 7.0f);
-    p = __builtin_fmaf(p, s2, 2.0f / 5.0f);
-    p = __builtin_fmaf(p, s2, 2.0f / 3.0f);
-    p = __builtin_fmaf(p, s2, 2.0f);
-    return s * p;
-}
-
-// Timescale of eq. 6: softplus(v) = max(v, 0) + log(1 + exp(-|v|)), or v
-// itself when the softplus flag is off.
-__device__ __forceinline__ float timescale(float v, bool softplus) {
-    if (!softplus) return v;
-    const float e = fast_exp2(-__builtin_fabsf(v) * kLog2e);
-    return __builtin_fmaxf(v, 0.0f) + log1p_unit(e);
-}
-
-// Cross-scan position maps. Direction k reads pixel pix(k, t) at position t:
-//   k = 0: t                         k = 2: L - 1 - t
-//   k = 1: (t % H) * W + t / H       k = 3: same as 1 at L - 1 - t
-__device__ __forceinline__ int pixel_of(int k, int t, int H, int W) {
-    const int L = H * W;
-    const int tt = (k >= 2) ? (L - 1 - t) : t;
-    if ((k & 1) == 0) return tt;
-    const int w = tt / H;
-    const int h = tt - w * H;
-    return h * W + w;
-}
-
 }  // namespace vmb
+
+#include "vmb_device.h"
