@@ -48,6 +48,8 @@ def _load():
     lib.oracle_mean_scan.restype = None
     lib.oracle_mean_scan_opt.argtypes = scan_args[:15] + [ctypes.c_int] + scan_args[15:]
     lib.oracle_mean_scan_opt.restype = None
+    lib.oracle_mean_scan_pooled.argtypes = scan_args[:13] + [P, ctypes.c_int]
+    lib.oracle_mean_scan_pooled.restype = None
     lib.oracle_cross_scan.argtypes = [P, P, I64, I64, I64, I64, I64]
     lib.oracle_cross_merge_f64.argtypes = [P, P, I64, I64, I64, I64]
     lib.oracle_cross_merge_f32.argtypes = [P, P, I64, I64, I64, I64]
@@ -143,6 +145,27 @@ def mean_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
     if sel is None:
         batch, K, Dc, L = np.shape(u)
         return y.reshape(batch, K, y.shape[1], L)
+    return y
+
+
+def mean_scan_pooled(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
+                     nthreads: int = 0) -> np.ndarray:
+    """VMeanba scan with T over all K*Dc channels of each batch element, fp64.
+
+    Inputs as for mean_scan. Returns the reduced output [batch, L]; the
+    method's output is this row broadcast to every (direction, channel).
+    """
+    lib = _load()
+    u, delta, A, B, C = map(_f32, (u, delta, A, B, C))
+    D, dt_bias = _f32(D), _f32(dt_bias)
+    batch, K, Dc, L = u.shape
+    N = A.shape[1]
+    assert delta.shape == u.shape and A.shape == (K * Dc, N)
+    assert B.shape == (batch, K, N, L) and C.shape == B.shape
+    y = np.empty((batch, L), dtype=np.float64)
+    lib.oracle_mean_scan_pooled(_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D),
+                                _ptr(dt_bias), int(bool(softplus)), batch, K, Dc, L, N, _ptr(y),
+                                int(nthreads))
     return y
 
 

@@ -231,6 +231,65 @@ void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, co
     }
 }
 
+/* VMeanba with T taken over every channel of an image: the K directions'
+ * channels pooled, K*Dc of them (Section 2.2, eq. 9, with the inner channel
+ * axis read as all K*Dc sequences of the image). Channel c = k*Dc + d carries
+ * its direction's B and C, so the channel means of the discretised terms are
+ *   abar[n,t] = mean_c exp(Delta_c,t A[c,n])
+ *   bu[n,t]   = mean_c Delta_c,t u_c,t B[b,k(c),n,t]
+ *   cbar[n,t] = mean_c C[b,k(c),n,t]
+ *   r[t]      = mean_c D[c] u_c,t
+ * and Mamba (eq. 3) runs once per batch element on them:
+ *   h[n] = abar h[n] + bu,   y[b,t] = sum_n cbar h[n] + r.
+ * Output y: [batch][L] (T^-1 broadcasts it to every (k, d)). */
+void oracle_mean_scan_pooled(const float* u, const float* delta, const float* A,
+                             const float* Bm, const float* Cm, const float* Ds,
+                             const float* dt_bias, int softplus, int64_t batch, int64_t K,
+                             int64_t Dc, int64_t L, int64_t N, double* y, int nthreads) {
+    set_threads(nthreads);
+#pragma omp parallel
+    {
+        double* h = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        double* abar = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        double* bu = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        double* cbar = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t b = 0; b < batch; ++b) {
+            const double inv = 1.0 / (double)(K * Dc);
+            for (int64_t n = 0; n < N; ++n) h[n] = 0.0;
+            for (int64_t t = 0; t < L; ++t) {
+                for (int64_t n = 0; n < N; ++n) abar[n] = bu[n] = cbar[n] = 0.0;
+                double r_sum = 0.0;
+                for (int64_t k = 0; k < K; ++k) {
+                    const int64_t bk = b * K + k;
+                    for (int64_t d = 0; d < Dc; ++d) {
+                        const int64_t c = k * Dc + d;
+                        const int64_t off = (bk * Dc + d) * L + t;
+                        const double dl = timescale((double)delta[off], dt_bias, c, softplus);
+                        const double ut = (double)u[off];
+                        for (int64_t n = 0; n < N; ++n) {
+                            abar[n] += exp(dl * (double)A[c * N + n]);
+                            bu[n] += dl * ut * (double)Bm[(bk * N + n) * L + t];
+                            cbar[n] += (double)Cm[(bk * N + n) * L + t];
+                        }
+                        r_sum += (Ds ? (double)Ds[c] : 0.0) * ut;
+                    }
+                }
+                double acc = 0.0;
+                for (int64_t n = 0; n < N; ++n) {
+                    h[n] = abar[n] * inv * h[n] + bu[n] * inv;
+                    acc += cbar[n] * inv * h[n];
+                }
+                y[b * L + t] = acc + r_sum * inv;
+            }
+        }
+        free(h);
+        free(abar);
+        free(bu);
+        free(cbar);
+    }
+}
+
 void oracle_mean_scan(const float* u, const float* delta, const float* A, const float* Bm,
                       const float* Cm, const float* Ds, const float* dt_bias, int softplus,
                       int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,

@@ -583,3 +583,78 @@ def test_discrete_scan_degenerate_sizes():
     abar, bu, C, _ = _discrete_case(44, batch=1, Dc=1, L=1, with_skip=False)
     y = oracle.discrete_scan(abar, bu, C)
     assert y.shape == (1, 1, 1) and y[0, 0, 0] == float(C[0, 0]) * float(bu[0, 0, 0])
+
+
+# ---------------------------------------------------------------- pooled reading (T over K*Dc)
+
+def run_pooled(c):
+    return oracle.mean_scan_pooled(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"],
+                                   c["dt_bias"], c["softplus"])
+
+
+def test_pooled_one_direction_is_direction_mean():
+    """K = 1: the image's channels are the direction's, so pooling changes nothing."""
+    c = rand_case(40, batch=2, K=1, Dc=5, L=9, N=3)
+    ref = run_mean(c)[:, 0, 0, :]
+    np.testing.assert_allclose(run_pooled(c), ref, rtol=1e-13, atol=1e-14)
+
+
+def test_pooled_identical_directions_is_direction_mean():
+    """Four identical directions (inputs, parameters, B and C): the mean over
+    all K*Dc channels is the mean over one direction's."""
+    c = rand_case(41, batch=2, K=4, Dc=3, L=8, N=3)
+    for key in ("u", "delta", "B", "C"):
+        c[key][...] = c[key][:, :1]
+    A = c["A"].reshape(4, 3, 3)
+    A[...] = A[:1]
+    for key in ("D", "dt_bias"):
+        v = c[key].reshape(4, 3)
+        v[...] = v[:1]
+    ref = run_mean(c)[:, 0, 0, :]
+    np.testing.assert_allclose(run_pooled(c), ref, rtol=1e-13, atol=1e-14)
+
+
+def test_pooled_identical_channels_is_full():
+    """Every channel of every direction identical, B and C shared by the
+    directions: the pooled scan is each channel's own full scan."""
+    c = rand_case(42, batch=1, K=4, Dc=3, L=10, N=2)
+    for key in ("u", "delta"):
+        c[key][...] = c[key][:, :1, :1]
+    for key in ("B", "C"):
+        c[key][...] = c[key][:, :1]
+    c["A"][...] = c["A"][:1]
+    for key in ("D", "dt_bias"):
+        c[key][...] = c[key][:1]
+    ref = run_full(c)[:, 0, 0, :]
+    np.testing.assert_allclose(run_pooled(c), ref, rtol=1e-13, atol=1e-14)
+
+
+def test_pooled_is_mean_of_full_when_timescale_and_c_shared():
+    """Delta and A shared by all K*Dc channels, C by the directions; u, D and
+    B (per direction) free. The recurrence is then linear in Delta u B with a
+    common decay, so the pooled output is exactly the mean of the full scan's
+    outputs over all K*Dc channels: this fixes how B, u and D enter."""
+    c = rand_case(43, batch=2, K=4, Dc=3, L=9, N=3)
+    c["delta"][...] = c["delta"][:, :1, :1]
+    c["A"][...] = c["A"][:1]
+    c["dt_bias"][...] = c["dt_bias"][:1]
+    c["C"][...] = c["C"][:, :1]
+    yf = run_full(c)
+    ref = yf.reshape(2, -1, 9).mean(axis=1)
+    np.testing.assert_allclose(run_pooled(c), ref, rtol=1e-12, atol=1e-13)
+
+
+def test_pooled_is_mean_of_full_when_only_c_differs():
+    """All channels identical except C, which differs per direction: every
+    channel has the same state, so the pooled output (the mean of C applied to
+    it) is the mean of the full outputs: this fixes how C enters."""
+    c = rand_case(44, batch=1, K=4, Dc=2, L=8, N=3)
+    for key in ("u", "delta"):
+        c[key][...] = c[key][:, :1, :1]
+    c["B"][...] = c["B"][:, :1]
+    c["A"][...] = c["A"][:1]
+    for key in ("D", "dt_bias"):
+        c[key][...] = c[key][:1]
+    yf = run_full(c)
+    ref = yf.reshape(1, -1, 8).mean(axis=1)
+    np.testing.assert_allclose(run_pooled(c), ref, rtol=1e-12, atol=1e-13)
