@@ -353,7 +353,8 @@ def variants_bench(steps: int, warmup: int):
     shape = workloads.STAGE1
     opts = {"main": 0, "skip_per_channel": vmb.VMB_MEAN_SKIP_PER_CHANNEL, "raw": vmb.VMB_MEAN_RAW,
             "no_broadcast": vmb.VMB_MEAN_NO_BROADCAST,
-            "raw_no_broadcast": vmb.VMB_MEAN_RAW | vmb.VMB_MEAN_NO_BROADCAST}
+            "raw_no_broadcast": vmb.VMB_MEAN_RAW | vmb.VMB_MEAN_NO_BROADCAST,
+            "pooled": vmb.VMB_MEAN_POOLED}
     rows = []
     for layout in ("seq", "2d"):
         inp = workloads.make_inputs(shape, layout)

@@ -178,7 +178,19 @@ typedef enum {
     VMB_MEAN_RAW = 2,
     /* T^-1 left out: y is [batch, K, 1, L] and holds ytilde (SEQ layout only;
      * not with VMB_MEAN_SKIP_PER_CHANNEL) */
-    VMB_MEAN_NO_BROADCAST = 4
+    VMB_MEAN_NO_BROADCAST = 4,
+    /* T over every channel of an image: the K directions' channels pooled
+     * (K*channels of them), each keeping its direction's B and C. With the
+     * sums over k and d (c = k*channels + d) and M = K*channels:
+     *   Abar_mean[n,t] = (1/M) sum_{k,d} exp(Delta_{k,d,t} A[c,n])
+     *   Bu_mean[n,t]   = (1/M) sum_k B[b,k,n,t] sum_d Delta_{k,d,t} u[b,k,d,t]
+     *   C_mean[n,t]    = (1/K) sum_k C[b,k,n,t]
+     *   r_mean[t]      = (1/M) sum_{k,d} D[c] u[b,k,d,t]
+     *   h_t[n] = Abar_mean[n,t] h_{t-1}[n] + Bu_mean[n,t],  ytilde_t = sum_n C_mean h_t[n] + r_mean
+     * one scan per batch element, broadcast to every (k, d); in the 2D layout
+     * the four directions' (identical) sequences are merged as usual. Only as
+     * the sole option bit. */
+    VMB_MEAN_POOLED = 8
 } vmb_mean_option;
 
 /*
@@ -187,7 +199,8 @@ typedef enum {
  * for vmb_mean_scan_fwd, except that y is [batch, K, 1, L] with
  * VMB_MEAN_NO_BROADCAST. Errors as for vmb_mean_scan_fwd, plus
  * VMB_ERR_UNSUPPORTED for an unknown bit, VMB_MEAN_NO_BROADCAST with the 2D
- * layout, or VMB_MEAN_NO_BROADCAST with VMB_MEAN_SKIP_PER_CHANNEL.
+ * layout, VMB_MEAN_NO_BROADCAST with VMB_MEAN_SKIP_PER_CHANNEL, or
+ * VMB_MEAN_POOLED with any other bit.
  */
 vmb_status vmb_mean_scan_fwd_ex(const void* u, const void* delta, const float* A, const void* B,
                                 const void* C, const float* D, const float* dt_bias,

@@ -660,6 +660,153 @@ unsigned long long next_epoch() {
     return e ? e : counter.fetch_add(2, std::memory_order_relaxed);
 }
 
+// ---------------------------------------------------------------- pooled reading
+// T over all K * channels sequences of an image (VMB_MEAN_POOLED). The
+// reduce of the main reading gives, per (b, k) and position, the sums over
+// the direction's channels of exp(Delta A_n), Delta u and D u; a direction's
+// B and C multiply its own sums, so the pooled means combine the directions:
+//   abar[n] = sum_k E_k[n] / M,  bu[n] = sum_k B_k[n] S_k / M,
+//   cbar[n] = sum_k C_k[n] / K,  r = sum_k R_k / M      (M = K * channels),
+// then one N-state scan per image (the one-state scan, states as channels)
+// and ytilde = sum_n cbar h + r, broadcast to every (k, d).
+
+// Pass 1: per chunk of one (b, k), the channel sums (fixed order over the
+// 16 channel groups), stored raw in psum[bk][row][t], rows 0..N-1 the exp
+// sums, N the Delta u sum, N + 1 the D u sum.
+template <int N, typename Tin, bool kTwoD>
+__global__ __launch_bounds__(kC* kRedWaves) void k_pooled_sums(
+    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
+    const float* __restrict__ D, const float* __restrict__ dt_bias, const Tin* __restrict__ xt,
+    float* __restrict__ psum, int K, int Dc, int L, int H, int W, int C, int softplus) {
+    __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
+    reduce_partials<N, Tin, kTwoD, false>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
+                                          softplus);
+    __syncthreads();
+    const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x % kC;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
+    const int t = chunk * C + lane;
+    if (lane >= C || t >= L) return;
+    const size_t bk = static_cast<size_t>(b) * K + k;
+    for (int row = wv; row < N + 2; row += kRedWaves) {
+        float sum = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) sum += part[w][row][lane];
+        psum[(bk * (N + 2) + row) * static_cast<size_t>(L) + t] = sum;
+    }
+}
+
+// Pass 2: the pooled scan inputs per (b, n, t) (state n = blockIdx.y),
+// directions added in order; the state-0 threads also form r and the ones.
+template <int N, typename Tin>
+__global__ __launch_bounds__(256) void k_pooled_combine(
+    const float* __restrict__ psum, const Tin* __restrict__ Bm, const Tin* __restrict__ Cm,
+    float* __restrict__ abar, float* __restrict__ bu, float* __restrict__ cbar,
+    float* __restrict__ ones, float* __restrict__ rbar, int K, int Dc, int L) {
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int n = blockIdx.y, b = blockIdx.z;
+    if (t >= L) return;
+    const float inv = 1.0f / (static_cast<float>(K) * static_cast<float>(Dc));
+    const float invk = 1.0f / static_cast<float>(K);
+    const size_t l = static_cast<size_t>(L);
+    float e = 0.0f, bs = 0.0f, cs = 0.0f, r = 0.0f;
+    for (int k = 0; k < K; ++k) {
+        const size_t bk = static_cast<size_t>(b) * K + k;
+        const float* ps = psum + bk * (N + 2) * l;
+        e += ps[n * l + t];
+        bs = __builtin_fmaf(to_f32(Bm[(bk * N + n) * l + t]), ps[N * l + t], bs);
+        cs += to_f32(Cm[(bk * N + n) * l + t]);
+        if (n == 0) r += ps[(N + 1) * l + t];
+    }
+    const size_t o = (static_cast<size_t>(b) * N + n) * l + t;
+    abar[o] = e * inv;
+    bu[o] = bs * inv;
+    cbar[o] = cs * invk;
+    if (n == 0) {
+        rbar[static_cast<size_t>(b) * l + t] = r * inv;
+        ones[static_cast<size_t>(b) * l + t] = 1.0f;
+    }
+}
+
+// Pass 4: ytilde = sum_n cbar h + r. Sequence layout: broadcast to the rows
+// (k, d) of row group blockIdx.y; 2-D layout (ytil4 given): the same value
+// written once per direction for the merge-and-broadcast pass.
+template <int N, typename Tout>
+__global__ __launch_bounds__(256) void k_pooled_out(const float* __restrict__ cbar,
+                                                    const float* __restrict__ h,
+                                                    const float* __restrict__ rbar,
+                                                    Tout* __restrict__ y,
+                                                    float* __restrict__ ytil4, int rows, int L,
+                                                    int groups) {
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int grp = blockIdx.y, b = blockIdx.z;
+    if (t >= L) return;
+    const size_t l = static_cast<size_t>(L);
+    float acc = rbar[static_cast<size_t>(b) * l + t];
+    for (int n = 0; n < N; ++n) {
+        const size_t o = (static_cast<size_t>(b) * N + n) * l + t;
+        acc = __builtin_fmaf(cbar[o], h[o], acc);
+    }
+    if (ytil4) {
+        for (int k = 0; k < 4; ++k) ytil4[(static_cast<size_t>(b) * 4 + k) * l + t] = acc;
+        return;
+    }
+    const int r0 = (grp * rows) / groups, r1 = ((grp + 1) * rows) / groups;
+    const Tout o = from_f32<Tout>(acc);
+    Tout* yb = y + static_cast<size_t>(b) * rows * l + t;
+    for (int r = r0; r < r1; ++r) yb[static_cast<size_t>(r) * l] = o;
+}
+
+template <int N, typename Tin, typename Tout, bool kTwoD>
+vmb_status run_pooled(const ScanArgs& a) {
+    const PooledWsLayout lay = pooled_ws_layout(a.batch, a.K, a.channels, a.L, N, kTwoD);
+    char* p = static_cast<char*>(a.ws);
+    auto f = [&](size_t off) { return reinterpret_cast<float*>(p + off); };
+    const int K = int(a.K), Dc = int(a.channels), L = int(a.L), H = int(a.H), W = int(a.W);
+    const int C = kC;
+    const int nchunks = (L + C - 1) / C;
+    const Tin* xt = nullptr;
+    if (kTwoD && mean_transposes(a.L, true) && cross_plane_fits(a.batch, a.channels, a.H, a.W)) {
+        vmb_status s0 = launch_transpose_planes(a.u, p + lay.xt, a.batch, a.channels, a.H, a.W,
+                                                a.in_dt, a.stream);
+        if (s0 != VMB_OK) return s0;
+        xt = reinterpret_cast<const Tin*>(p + lay.xt);
+    }
+    hipLaunchKernelGGL((k_pooled_sums<N, Tin, kTwoD>),
+                       dim3(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch)),
+                       dim3(kC * kRedWaves), 0, a.stream, static_cast<const Tin*>(a.u),
+                       static_cast<const Tin*>(a.delta), a.A, a.D, a.dt_bias, xt, f(lay.psum), K,
+                       Dc, L, H, W, C, a.softplus);
+    vmb_status st = check_launch();
+    if (st != VMB_OK) return st;
+    const unsigned pblk = static_cast<unsigned>((L + 255) / 256);
+    hipLaunchKernelGGL((k_pooled_combine<N, Tin>), dim3(pblk, N, static_cast<unsigned>(a.batch)),
+                       dim3(256), 0, a.stream, f(lay.psum), static_cast<const Tin*>(a.B),
+                       static_cast<const Tin*>(a.C), f(lay.abar), f(lay.bu), f(lay.cbar),
+                       f(lay.ones), f(lay.rbar), K, Dc, L);
+    st = check_launch();
+    if (st != VMB_OK) return st;
+    // the states of the pooled scan: one-state scans with the states as channels
+    st = launch_discrete_scan(f(lay.abar), f(lay.bu), f(lay.ones), nullptr, f(lay.h), a.batch, N,
+                              a.L, a.stream);
+    if (st != VMB_OK) return st;
+    const int rows = K * Dc;
+    if (kTwoD) {
+        hipLaunchKernelGGL((k_pooled_out<N, Tout>), dim3(pblk, 1, static_cast<unsigned>(a.batch)),
+                           dim3(256), 0, a.stream, f(lay.cbar), f(lay.h), f(lay.rbar),
+                           static_cast<Tout*>(nullptr), f(lay.ytil), rows, L, 1);
+        st = check_launch();
+        if (st != VMB_OK) return st;
+        return launch_merge_broadcast<Tin, Tout>(f(lay.ytil), a);
+    }
+    const long long want = (1024 + pblk * a.batch - 1) / (pblk * a.batch);
+    const int groups = clamp_groups(want, rows);
+    hipLaunchKernelGGL((k_pooled_out<N, Tout>),
+                       dim3(pblk, static_cast<unsigned>(groups), static_cast<unsigned>(a.batch)),
+                       dim3(256), 0, a.stream, f(lay.cbar), f(lay.h), f(lay.rbar),
+                       static_cast<Tout*>(a.y), static_cast<float*>(nullptr), rows, L, groups);
+    return check_launch();
+}
+
 template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw>
 vmb_status run(const ScanArgs& a) {
     const size_t bkn = static_cast<size_t>(a.batch * a.K);
@@ -745,6 +892,9 @@ vmb_status dispatch_layout(const ScanArgs& a) {
 
 template <int N, typename Tin, typename Tout>
 vmb_status dispatch_reading(const ScanArgs& a) {
+    if (a.options & VMB_MEAN_POOLED)
+        return a.layout == VMB_LAYOUT_SEQ ? run_pooled<N, Tin, Tout, false>(a)
+                                          : run_pooled<N, Tin, Tout, true>(a);
     return (a.options & VMB_MEAN_RAW) ? dispatch_layout<N, Tin, Tout, true>(a)
                                       : dispatch_layout<N, Tin, Tout, false>(a);
 }

@@ -87,6 +87,35 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, i
     return o;
 }
 
+// Workspace of the pooled reading (VMB_MEAN_POOLED), 256-byte aligned regions:
+//   psum  [bk][N+2][L] : per-direction channel sums (exp sums per state, Delta u, D u)
+//   abar, bu, cbar, h [batch][N][L] : the pooled scan's inputs, C_mean and its states
+//   ones  [batch][L]   : the scan's output coefficient (its states are wanted as they are)
+//   rbar  [batch][L]   : pooled skip term
+//   ytil  [batch][4][L]: ytilde written once per direction (2-D merge input)
+//   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL, as in the main reading
+struct PooledWsLayout {
+    size_t psum, abar, bu, cbar, h, ones, rbar, ytil, xt, total;
+};
+inline PooledWsLayout pooled_ws_layout(int64_t batch, int64_t K, int64_t channels, int64_t L,
+                                       int64_t N, bool two_d) {
+    auto up = [](size_t v) { return (v + 255) & ~size_t{255}; };
+    const size_t bk = static_cast<size_t>(batch) * static_cast<size_t>(K);
+    const size_t b = static_cast<size_t>(batch), l = static_cast<size_t>(L), n = static_cast<size_t>(N);
+    PooledWsLayout o;
+    o.psum = 0;
+    o.abar = o.psum + up(bk * (n + 2) * l * 4);
+    o.bu = o.abar + up(b * n * l * 4);
+    o.cbar = o.bu + up(b * n * l * 4);
+    o.h = o.cbar + up(b * n * l * 4);
+    o.ones = o.h + up(b * n * l * 4);
+    o.rbar = o.ones + up(b * l * 4);
+    o.ytil = o.rbar + up(b * l * 4);
+    o.xt = o.ytil + up(b * 4 * l * 4);
+    o.total = o.xt + (mean_transposes(L, two_d) ? up(b * static_cast<size_t>(channels) * l * 4) : 0);
+    return o;
+}
+
 // Launchers (enqueue only; arguments already validated).
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
                              int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);

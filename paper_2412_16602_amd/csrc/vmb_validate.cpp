@@ -105,7 +105,10 @@ size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t 
         if (full_ws_has_xt(batch, K, channels, L, N)) bytes += full_ws_xt_bytes(batch, channels, L);
         return bytes;
     }
-    return mean_ws_layout(batch, K, channels, L, N, layout == VMB_LAYOUT_2D).total;
+    // room for the main reading and for the pooled one (VMB_MEAN_POOLED)
+    const size_t main = mean_ws_layout(batch, K, channels, L, N, layout == VMB_LAYOUT_2D).total;
+    const size_t pooled = pooled_ws_layout(batch, K, channels, L, N, layout == VMB_LAYOUT_2D).total;
+    return main > pooled ? main : pooled;
 }
 
 vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
@@ -125,8 +128,10 @@ vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
         if (a.K != 4 || a.H < 1 || a.W < 1 || prod({a.H, a.W}) != a.L) return VMB_ERR_SHAPE;
     }
     if (!supported_n(a.N)) return VMB_ERR_UNSUPPORTED;
-    const unsigned known = VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST;
+    const unsigned known =
+        VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST | VMB_MEAN_POOLED;
     if (a.options & ~known) return VMB_ERR_UNSUPPORTED;
+    if ((a.options & VMB_MEAN_POOLED) && a.options != VMB_MEAN_POOLED) return VMB_ERR_UNSUPPORTED;
     if (a.options && !mean_variant) return VMB_ERR_UNSUPPORTED;
     const bool no_bcast = (a.options & VMB_MEAN_NO_BROADCAST) != 0;
     if (no_bcast && (a.layout != VMB_LAYOUT_SEQ || (a.options & VMB_MEAN_SKIP_PER_CHANNEL)))

@@ -23,7 +23,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "vmb.h")
 VMB_F32, VMB_BF16 = 0, 1
 VMB_LAYOUT_SEQ, VMB_LAYOUT_2D = 0, 1
 # vmb_mean_option bits (vmb_mean_scan_fwd_ex)
-VMB_MEAN_SKIP_PER_CHANNEL, VMB_MEAN_RAW, VMB_MEAN_NO_BROADCAST = 1, 2, 4
+VMB_MEAN_SKIP_PER_CHANNEL, VMB_MEAN_RAW, VMB_MEAN_NO_BROADCAST, VMB_MEAN_POOLED = 1, 2, 4, 8
 
 STATUS = {0: "VMB_OK", 1: "VMB_ERR_NULL", 2: "VMB_ERR_SHAPE", 3: "VMB_ERR_DTYPE",
           4: "VMB_ERR_ALIGN", 5: "VMB_ERR_ALIAS", 6: "VMB_ERR_UNSUPPORTED",

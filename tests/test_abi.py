@@ -82,18 +82,24 @@ def test_scan_rejects(lib, fn, kw, expect):
 def test_mean_options_rules(lib):
     ex = "vmb_mean_scan_fwd_ex"
     SKIP1, RAW, NOBC = vmb.VMB_MEAN_SKIP_PER_CHANNEL, vmb.VMB_MEAN_RAW, vmb.VMB_MEAN_NO_BROADCAST
+    POOL = vmb.VMB_MEAN_POOLED
     # the descriptions of include/vmb.h carry the same values
     with open(vmb.HEADER_PATH) as f:
         text = f.read()
     for name, val in (("VMB_MEAN_SKIP_PER_CHANNEL", SKIP1), ("VMB_MEAN_RAW", RAW),
-                      ("VMB_MEAN_NO_BROADCAST", NOBC)):
+                      ("VMB_MEAN_NO_BROADCAST", NOBC), ("VMB_MEAN_POOLED", POOL)):
         assert f"{name} = {val}" in text
     # a call that passes validation reaches the launch, which fails on a host
     # without a GPU (VMB_ERR_HIP): the status says validation let it through
     passed = (OK, 8)
     for opt in (0, SKIP1, RAW, NOBC, SKIP1 | RAW, RAW | NOBC):
         assert scan_call(lib, ex, options=opt) in passed
-    assert scan_call(lib, ex, options=8) == UNSUP
+    assert scan_call(lib, ex, options=16) == UNSUP
+    # the pooled reading only on its own, in either layout
+    assert scan_call(lib, ex, options=POOL) in passed
+    assert scan_call(lib, ex, options=POOL, layout=TWO_D) in passed
+    for other in (SKIP1, RAW, NOBC):
+        assert scan_call(lib, ex, options=POOL | other) == UNSUP
     assert scan_call(lib, ex, options=NOBC | SKIP1) == UNSUP
     assert scan_call(lib, ex, options=NOBC, layout=TWO_D) == UNSUP
     assert scan_call(lib, ex, options=SKIP1 | RAW, layout=TWO_D) in passed
