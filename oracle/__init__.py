@@ -44,6 +44,8 @@ def _load():
     scan_args = [P, P, P, P, P, P, P, ctypes.c_int, I64, I64, I64, I64, I64, P, I64, P, ctypes.c_int]
     lib.oracle_full_scan.argtypes = scan_args
     lib.oracle_full_scan.restype = None
+    lib.oracle_full_scan_opt.argtypes = scan_args[:15] + [ctypes.c_int] + scan_args[15:]
+    lib.oracle_full_scan_opt.restype = None
     lib.oracle_mean_scan.argtypes = scan_args
     lib.oracle_mean_scan.restype = None
     lib.oracle_mean_scan_opt.argtypes = scan_args[:15] + [ctypes.c_int] + scan_args[15:]
@@ -82,6 +84,9 @@ def max_threads() -> int:
 MEAN_SKIP_PER_CHANNEL = 1  # D u outside T, added per channel after the broadcast
 MEAN_RAW = 2               # T averages Delta, u and A before the discretisation
 MEAN_NO_BROADCAST = 4      # T^-1 left out: one reduced row per (batch, k)
+# zero-order-hold B-bar (eq. 4, second line as (delta A)^-1 (exp(delta A) - I) delta B),
+# for full_scan and mean_scan alike
+ZOH = 16
 
 
 def _scan(fn_name, per_seq, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads,
@@ -110,14 +115,21 @@ def _scan(fn_name, per_seq, u, delta, A, B, C, D, dt_bias, softplus, sel, nthrea
 
 
 def full_scan(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
-              sel: Optional[Sequence[int]] = None, nthreads: int = 0) -> np.ndarray:
+              sel: Optional[Sequence[int]] = None, nthreads: int = 0,
+              options: int = 0) -> np.ndarray:
     """Full selective scan in fp64.
 
     u, delta: [batch, K, Dc, L]; A: [K*Dc, N]; B, C: [batch, K, N, L];
     D, dt_bias: [K*Dc] or None. Returns [batch, K, Dc, L] (sel None) or
     [len(sel), L] for the flat sequence indices (b*K + k)*Dc + d in ``sel``.
+    ``options`` ZOH selects the zero-order-hold B-bar.
     """
-    y = _scan("oracle_full_scan", True, u, delta, A, B, C, D, dt_bias, softplus, sel, nthreads)
+    if options:
+        y = _scan("oracle_full_scan_opt", True, u, delta, A, B, C, D, dt_bias, softplus, sel,
+                  nthreads, options=options)
+    else:
+        y = _scan("oracle_full_scan", True, u, delta, A, B, C, D, dt_bias, softplus, sel,
+                  nthreads)
     if sel is None:
         return y.reshape(np.shape(u))
     return y

@@ -19,7 +19,10 @@
  * Readings where the paper is silent or garbled (all arithmetic in double on
  * the exact input values):
  *   - B-bar u is the first-order form delta * B * u (eq. 4's second line is
- *     garbled in the paper); C is used undiscretised.
+ *     garbled in the paper); C is used undiscretised. Option bit 16 of the
+ *     *_opt functions takes eq. 4's second line as zero-order hold instead,
+ *     (delta A)^-1 (exp(delta A) - I) delta B, i.e. B-bar u =
+ *     phi(delta A) delta B u with phi(x) = (e^x - 1) / x (phi(0) = 1).
  *   - h starts at zero; no final state is returned.
  *   - T averages exp(delta*A) and delta*B*u over the channels of one
  *     direction; C carries no channel axis so T leaves it unchanged; the skip
@@ -80,11 +83,20 @@ int oracle_max_threads(void) {
  *   h_t    = Abar * h_{t-1} + Delta_t * B[n, t] * u_t
  *   y_t    = sum_n C[n, t] * h_t + D[c] * u_t
  */
-void oracle_full_scan(const float* u, const float* delta, const float* A, const float* Bm,
-                      const float* Cm, const float* Ds, const float* dt_bias, int softplus,
-                      int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,
-                      const int64_t* sel, int64_t nsel, double* y, int nthreads) {
-    (void)batch;
+/* The zero-order-hold gain of eq. 4, second line: (e^x - 1) / x at x = delta * A
+ * (the limit 1 at x = 0), so that B-bar = gain * delta * B. */
+static double zoh_gain(double x) { return x == 0.0 ? 1.0 : expm1(x) / x; }
+
+/*
+ * Full scan with option bits: 16 = zero-order-hold B-bar (see the header);
+ * otherwise as oracle_full_scan.
+ */
+void oracle_full_scan_opt(const float* u, const float* delta, const float* A, const float* Bm,
+                          const float* Cm, const float* Ds, const float* dt_bias, int softplus,
+                          int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,
+                          const int64_t* sel, int64_t nsel, int options, double* y,
+                          int nthreads) {
+    const int zoh = (options & 16) != 0;
     set_threads(nthreads);
     if (!sel) nsel = batch * K * Dc;
 #pragma omp parallel
@@ -108,8 +120,10 @@ void oracle_full_scan(const float* u, const float* delta, const float* A, const 
                 const double ut = (double)us[t];
                 double acc = 0.0;
                 for (int64_t n = 0; n < N; ++n) {
-                    const double abar = exp(dl * (double)A[c * N + n]);
-                    const double bu = dl * (double)Bs[n * L + t] * ut;
+                    const double x = dl * (double)A[c * N + n];
+                    const double abar = exp(x);
+                    const double gain = zoh ? zoh_gain(x) : 1.0;
+                    const double bu = gain * dl * (double)Bs[n * L + t] * ut;
                     h[n] = abar * h[n] + bu;
                     acc += (double)Cs[n * L + t] * h[n];
                 }
@@ -118,6 +132,21 @@ void oracle_full_scan(const float* u, const float* delta, const float* A, const 
         }
         free(h);
     }
+}
+
+/*
+ * Full selective scan, eq. 3 for every (b, k, d, n), c = k*Dc + d:
+ *   Delta_t = softplus(delta_t + dt_bias[c])           (eq. 6)
+ *   h_t[n]  = exp(Delta_t A[c,n]) h_{t-1}[n] + Delta_t B[b,k,n,t] u_t   (eq. 4, first line)
+ *   y_t     = sum_n C[b,k,n,t] h_t[n] + D[c] u_t
+ * sel lists flat sequence indices (b*K + k)*Dc + d (NULL: all); y is [nsel, L].
+ */
+void oracle_full_scan(const float* u, const float* delta, const float* A, const float* Bm,
+                      const float* Cm, const float* Ds, const float* dt_bias, int softplus,
+                      int64_t batch, int64_t K, int64_t Dc, int64_t L, int64_t N,
+                      const int64_t* sel, int64_t nsel, double* y, int nthreads) {
+    oracle_full_scan_opt(u, delta, A, Bm, Cm, Ds, dt_bias, softplus, batch, K, Dc, L, N, sel,
+                         nsel, 0, y, nthreads);
 }
 
 /*
@@ -147,6 +176,11 @@ void oracle_full_scan(const float* u, const float* delta, const float* A, const 
  *      (the skip term as above, r_mean or per channel)
  *   4  no broadcast: T^-1 is left out and y receives [nsel, L], the reduced
  *      output ytilde of each (b, k) (not with option 1)
+ *   16 zero-order-hold B-bar (see the header): T averages
+ *        phi(Delta_{d,t} A[c,n]) Delta_{d,t} u_{d,t} per state n,
+ *      h_t = Abar_mean[n,t] h_{t-1} + B[n,t] (1/Dc) sum_d phi(..) Delta u;
+ *      with option 2 the means are discretised with it:
+ *      phi(Delta_mean A_mean[n]) Delta_mean B[n,t] u_mean
  */
 void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, const float* Bm,
                           const float* Cm, const float* Ds, const float* dt_bias, int softplus,
@@ -156,6 +190,7 @@ void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, co
     const int skip_per_channel = (options & 1) != 0;
     const int raw_mean = (options & 2) != 0;
     const int broadcast = (options & 4) == 0;
+    const int zoh = (options & 16) != 0;
     set_threads(nthreads);
     if (!sel) nsel = batch * K;
 #pragma omp parallel
@@ -163,6 +198,7 @@ void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, co
         double* h = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
         double* abar = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
         double* amean = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        double* zsum = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
 #pragma omp for schedule(dynamic, 1)
         for (int64_t i = 0; i < nsel; ++i) {
             const int64_t bk = sel ? sel[i] : i;
@@ -179,14 +215,18 @@ void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, co
             for (int64_t n = 0; n < N; ++n) h[n] = 0.0;
             for (int64_t t = 0; t < L; ++t) {
                 /* T: mean over the inner channel axis */
-                for (int64_t n = 0; n < N; ++n) abar[n] = 0.0;
+                for (int64_t n = 0; n < N; ++n) abar[n] = zsum[n] = 0.0;
                 double s_sum = 0.0, r_sum = 0.0, dl_sum = 0.0, u_sum = 0.0;
                 for (int64_t d = 0; d < Dc; ++d) {
                     const int64_t c = k * Dc + d;
                     const int64_t off = (bk * Dc + d) * L + t;
                     const double dl = timescale((double)delta[off], dt_bias, c, softplus);
                     const double ut = (double)u[off];
-                    for (int64_t n = 0; n < N; ++n) abar[n] += exp(dl * (double)A[c * N + n]);
+                    for (int64_t n = 0; n < N; ++n) {
+                        const double x = dl * (double)A[c * N + n];
+                        abar[n] += exp(x);
+                        zsum[n] += zoh_gain(x) * dl * ut;
+                    }
                     s_sum += dl * ut;
                     r_sum += (Ds ? (double)Ds[c] : 0.0) * ut;
                     dl_sum += dl;
@@ -201,11 +241,11 @@ void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, co
                         /* eq. 4 applied to the means */
                         const double dm = dl_sum * inv, um = u_sum * inv;
                         a_n = exp(dm * amean[n]);
-                        bu_n = dm * (double)Bs[n * L + t] * um;
+                        bu_n = (zoh ? zoh_gain(dm * amean[n]) : 1.0) * dm * (double)Bs[n * L + t] * um;
                     } else {
                         /* the means of the discretised terms */
                         a_n = abar[n] * inv;
-                        bu_n = (double)Bs[n * L + t] * (s_sum * inv);
+                        bu_n = (double)Bs[n * L + t] * ((zoh ? zsum[n] : s_sum) * inv);
                     }
                     h[n] = a_n * h[n] + bu_n;
                     acc += (double)Cs[n * L + t] * h[n];
@@ -226,6 +266,7 @@ void oracle_mean_scan_opt(const float* u, const float* delta, const float* A, co
             }
         }
         free(amean);
+        free(zsum);
         free(abar);
         free(h);
     }

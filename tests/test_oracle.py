@@ -658,3 +658,90 @@ def test_pooled_is_mean_of_full_when_only_c_differs():
     yf = run_full(c)
     ref = yf.reshape(1, -1, 8).mean(axis=1)
     np.testing.assert_allclose(run_pooled(c), ref, rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- zero-order hold (eq. 4)
+
+def test_zoh_is_exact_step_of_the_ode():
+    """With u, B and Delta held over a step, ZOH is the exact solution of
+    h' = A h + B u (eq. 1): each step equals the matrix exponential of the
+    augmented system [[A, B u], [0, 0]] * Delta (Van Loan), by scipy."""
+    import scipy.linalg
+    c = rand_case(50, batch=1, K=1, Dc=2, L=6, N=3)
+    y = oracle.full_scan(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"], c["dt_bias"],
+                         True, options=oracle.ZOH)
+    dl = timescale_np(c["delta"], c["dt_bias"], True, 1, 2)
+    for d in range(2):
+        h = np.zeros(3)
+        for t in range(6):
+            acc = 0.0
+            for n in range(3):
+                a = float(c["A"][d, n])
+                bu = float(c["B"][0, 0, n, t]) * float(c["u"][0, 0, d, t])
+                M = np.array([[a, bu], [0.0, 0.0]]) * dl[0, 0, d, t]
+                E = scipy.linalg.expm(M)
+                h[n] = E[0, 0] * h[n] + E[0, 1]
+                acc += float(c["C"][0, 0, n, t]) * h[n]
+            ref = acc + float(c["D"][d]) * float(c["u"][0, 0, d, t])
+            assert abs(y[0, 0, d, t] - ref) <= 1e-12 * max(1.0, abs(ref))
+
+
+def test_zoh_constant_inputs_closed_form():
+    """Constant Delta, A, B, u: h_t = a h_{t-1} + (a - 1) B u / A sums to
+    h_t = (a^(t+1) - 1) B u / A, which tends to the steady state -B u / A."""
+    L = 40
+    u = np.full((1, 1, 1, L), 0.7, np.float32)
+    delta = np.full((1, 1, 1, L), 0.25, np.float32)
+    A = np.array([[-1.5]], np.float32)
+    B = np.full((1, 1, 1, L), 1.3, np.float32)
+    C = np.ones((1, 1, 1, L), np.float32)
+    y = oracle.full_scan(u, delta, A, B, C, None, None, False, options=oracle.ZOH)[0, 0, 0]
+    a = math.exp(0.25 * -1.5)
+    bu_over_a = float(np.float32(1.3)) * float(np.float32(0.7)) / -1.5
+    for t in range(L):
+        ref = (a ** (t + 1) - 1.0) * bu_over_a
+        assert abs(y[t] - ref) <= 1e-13
+    assert abs(y[-1] + bu_over_a) < 1e-6  # steady state -B u / A
+
+
+def test_zoh_tends_to_euler_as_a_vanishes():
+    """phi(x) = (e^x - 1)/x -> 1 as x -> 0: with a tiny A the two B-bar forms agree."""
+    c = rand_case(51, batch=1, K=2, Dc=2, L=8, N=2)
+    c["A"][...] = -1e-7
+    ze = oracle.full_scan(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"], c["dt_bias"],
+                          True, options=oracle.ZOH)
+    eu = run_full(c)
+    np.testing.assert_allclose(ze, eu, rtol=1e-6, atol=1e-9)
+    assert not np.array_equal(ze, eu)
+
+
+def test_zoh_mean_equals_full_when_channels_identical():
+    c = rand_case(52, batch=2, K=2, Dc=4, L=9, N=3)
+    for key in ("u", "delta"):
+        c[key][...] = c[key][:, :, :1, :]
+    A = c["A"].reshape(2, 4, 3)
+    A[...] = A[:, :1, :]
+    for key in ("D", "dt_bias"):
+        v = c[key].reshape(2, 4)
+        v[...] = v[:, :1]
+    ym = run_mean(c, options=oracle.ZOH)
+    yf = oracle.full_scan(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"], c["dt_bias"],
+                          True, options=oracle.ZOH)
+    np.testing.assert_allclose(ym, yf, rtol=1e-13, atol=1e-14)
+
+
+def test_zoh_mean_is_channel_mean_of_full_when_timescale_shared():
+    """Delta and A shared by a direction's channels: the ZOH gain is then
+    common too, the recurrence linear in u, and the reduced output the channel
+    mean of the full ZOH outputs."""
+    c = rand_case(53, batch=1, K=3, Dc=5, L=10, N=3)
+    c["delta"][...] = c["delta"][:, :, :1, :]
+    A = c["A"].reshape(3, 5, 3)
+    A[...] = A[:, :1, :]
+    v = c["dt_bias"].reshape(3, 5)
+    v[...] = v[:, :1]
+    ym = run_mean(c, options=oracle.ZOH)
+    yf = oracle.full_scan(c["u"], c["delta"], c["A"], c["B"], c["C"], c["D"], c["dt_bias"],
+                          True, options=oracle.ZOH)
+    ref = np.broadcast_to(yf.mean(axis=2, keepdims=True), yf.shape)
+    np.testing.assert_allclose(ym, ref, rtol=1e-12, atol=1e-13)
