@@ -136,6 +136,35 @@ vmb_status vmb_selective_scan_fwd(const void* u, const void* delta, const float*
                                   size_t workspace_bytes, vmb_stream_t stream);
 
 /*
+ * Options of vmb_selective_scan_fwd_ex (bit flags; vmb_mean_scan_fwd_ex
+ * takes them too, next to its vmb_mean_option bits).
+ */
+typedef enum {
+    /* Eq. 4's second line read as zero-order hold,
+     *   Bbar = (Delta A)^-1 (exp(Delta A) - I) Delta B,
+     * i.e. Bbar u = phi(Delta A[c,n]) Delta B[b,k,n,t] u with
+     * phi(x) = (e^x - 1) / x (phi(0) = 1), in place of the first-order
+     * Delta B u; Abar = exp(Delta A) as before. Under the mean (T of eq. 9)
+     * the per-state means (1/channels) sum_d phi(Delta_d A[c,n]) Delta_d u_d
+     * take the place of mean_d Delta_d u_d. */
+    VMB_SCAN_ZOH = 16
+} vmb_scan_option;
+
+/*
+ * vmb_selective_scan_fwd with options (a bitwise OR of vmb_scan_option
+ * values; 0 is vmb_selective_scan_fwd). Arguments, workspace and errors as for
+ * vmb_selective_scan_fwd, plus VMB_ERR_UNSUPPORTED for an unknown bit.
+ */
+vmb_status vmb_selective_scan_fwd_ex(const void* u, const void* delta, const float* A,
+                                     const void* B, const void* C, const float* D,
+                                     const float* dt_bias, int delta_softplus, void* y,
+                                     int64_t batch, int64_t K, int64_t channels, int64_t L,
+                                     int64_t N, vmb_dtype in_dtype, vmb_dtype out_dtype,
+                                     vmb_layout layout, int64_t H, int64_t W, void* workspace,
+                                     size_t workspace_bytes, unsigned options,
+                                     vmb_stream_t stream);
+
+/*
  * VMeanba scan (Section 2.2, eq. 9): T averages the discretised scan inputs
  * over the channels of each direction, the scan runs once per (b, k), and
  * T^-1 broadcasts its output to every channel. With Delta as above and the
@@ -200,7 +229,8 @@ typedef enum {
  * VMB_MEAN_NO_BROADCAST. Errors as for vmb_mean_scan_fwd, plus
  * VMB_ERR_UNSUPPORTED for an unknown bit, VMB_MEAN_NO_BROADCAST with the 2D
  * layout, VMB_MEAN_NO_BROADCAST with VMB_MEAN_SKIP_PER_CHANNEL, or
- * VMB_MEAN_POOLED with any other bit.
+ * VMB_MEAN_POOLED with any other bit. VMB_SCAN_ZOH (vmb_scan_option) may be
+ * added to 0, VMB_MEAN_SKIP_PER_CHANNEL or VMB_MEAN_NO_BROADCAST.
  */
 vmb_status vmb_mean_scan_fwd_ex(const void* u, const void* delta, const float* A, const void* B,
                                 const void* C, const float* D, const float* dt_bias,

@@ -73,6 +73,22 @@ vmb_status vmb_selective_scan_fwd(const void* u, const void* delta, const float*
     return launch_full_scan(a);
 }
 
+vmb_status vmb_selective_scan_fwd_ex(const void* u, const void* delta, const float* A,
+                                     const void* B, const void* C, const float* D,
+                                     const float* dt_bias, int delta_softplus, void* y,
+                                     int64_t batch, int64_t K, int64_t channels, int64_t L,
+                                     int64_t N, vmb_dtype in_dtype, vmb_dtype out_dtype,
+                                     vmb_layout layout, int64_t H, int64_t W, void* workspace,
+                                     size_t workspace_bytes, unsigned options,
+                                     vmb_stream_t stream) {
+    ScanArgs a = pack(u, delta, A, B, C, D, dt_bias, delta_softplus, y, batch, K, channels, L, N,
+                      in_dtype, out_dtype, layout, H, W, workspace, workspace_bytes, stream);
+    a.options = options;
+    const vmb_status st = validate_scan(a, 0);
+    if (st != VMB_OK) return st;
+    return launch_full_scan(a);
+}
+
 vmb_status vmb_mean_scan_fwd(const void* u, const void* delta, const float* A, const void* B,
                              const void* C, const float* D, const float* dt_bias,
                              int delta_softplus, void* y, int64_t batch, int64_t K,

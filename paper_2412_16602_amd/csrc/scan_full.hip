@@ -20,7 +20,7 @@ namespace {
 
 constexpr int kWave = 64;
 
-template <int N, typename Tin, typename Tout, bool kTwoD>
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kZoh>
 __global__ __launch_bounds__(kWave) void k_full_scan_lanes(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
@@ -34,9 +34,12 @@ __global__ __launch_bounds__(kWave) void k_full_scan_lanes(
     const size_t bk = static_cast<size_t>(b) * K + k;
     const size_t row = (bk * Dc + d) * static_cast<size_t>(L);
 
-    float a_row[N];
+    float a_row[N], inv_a[N];
 #pragma unroll
-    for (int n = 0; n < N; ++n) a_row[n] = A[static_cast<size_t>(c) * N + n];
+    for (int n = 0; n < N; ++n) {
+        a_row[n] = A[static_cast<size_t>(c) * N + n];
+        inv_a[n] = kZoh ? 1.0f / a_row[n] : 0.0f;
+    }
     const float bias = dt_bias ? dt_bias[c] : 0.0f;
     const float dskip = D ? D[c] : 0.0f;
     const bool sp = softplus != 0;
@@ -60,8 +63,10 @@ __global__ __launch_bounds__(kWave) void k_full_scan_lanes(
         float acc = dskip * ut;
 #pragma unroll
         for (int n = 0; n < N; ++n) {
-            const float a = fast_exp2(dl2 * a_row[n]);
-            const float bu = du * to_f32(Bb[n * L + t]);
+            const float x2 = dl2 * a_row[n];
+            const float a = fast_exp2(x2);
+            const float q = kZoh ? zoh_q(x2, a, du, ut, inv_a[n]) : du;
+            const float bu = q * to_f32(Bb[n * L + t]);
             h[n] = __builtin_fmaf(a, h[n], bu);
             acc = __builtin_fmaf(to_f32(Cb[n * L + t]), h[n], acc);
         }
@@ -69,15 +74,21 @@ __global__ __launch_bounds__(kWave) void k_full_scan_lanes(
     }
 }
 
-template <int N, typename Tin, typename Tout, bool kTwoD>
-vmb_status launch_lanes(const ScanArgs& a, Tout* y) {
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kZoh>
+vmb_status launch_lanes_zoh(const ScanArgs& a, Tout* y) {
     const dim3 grid(static_cast<unsigned>((a.channels + kWave - 1) / kWave),
                     static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
-    hipLaunchKernelGGL((k_full_scan_lanes<N, Tin, Tout, kTwoD>), grid, dim3(kWave), 0, a.stream,
+    hipLaunchKernelGGL((k_full_scan_lanes<N, Tin, Tout, kTwoD, kZoh>), grid, dim3(kWave), 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,
                        y, int(a.K), int(a.channels), int(a.L), int(a.H), int(a.W), a.softplus);
     return check_launch();
+}
+
+template <int N, typename Tin, typename Tout, bool kTwoD>
+vmb_status launch_lanes(const ScanArgs& a, Tout* y) {
+    return (a.options & VMB_SCAN_ZOH) ? launch_lanes_zoh<N, Tin, Tout, kTwoD, true>(a, y)
+                                      : launch_lanes_zoh<N, Tin, Tout, kTwoD, false>(a, y);
 }
 
 template <int N, typename Tin, typename Tout>
@@ -102,16 +113,20 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L > kShortMaxL; }
 
 vmb_status launch_full_scan(const ScanArgs& a) {
-    if (use_tiles_full(a) || use_chunked_full(a) || use_short_full(a)) {
+    // the zero-order-hold B runs in the tile kernel (N = 16) or the lane
+    // kernel (other shapes) only
+    const bool zoh = (a.options & VMB_SCAN_ZOH) != 0;
+    const bool tiles = zoh ? tiles_take(a) : use_tiles_full(a);
+    if (tiles || (!zoh && (use_chunked_full(a) || use_short_full(a)))) {
         auto run = [&](void* y_seq, const void* xt) {
-            if (use_tiles_full(a)) return launch_full_tiles(a, y_seq, xt);
+            if (tiles) return launch_full_tiles(a, y_seq, xt);
             return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq);
         };
         if (a.layout == VMB_LAYOUT_SEQ) return run(a.y, nullptr);
         // 2-D: the tile path reads directions 1 and 3 from column-major plane
         // copies in the workspace
         const void* xt = nullptr;
-        if (use_tiles_full(a) && full_ws_has_xt(a.batch, a.K, a.channels, a.L, a.N)) {
+        if (tiles && full_ws_has_xt(a.batch, a.K, a.channels, a.L, a.N)) {
             void* xtw = static_cast<char*>(a.ws) + full_ws_xt_offset(a.batch, a.K, a.channels, a.L);
             vmb_status st = launch_transpose_planes(a.u, xtw, a.batch, a.channels, a.H, a.W,
                                                     a.in_dt, a.stream);

@@ -105,7 +105,7 @@ __device__ __forceinline__ void row8(const bf16_t* r, int off, float (&v)[8]) {
     }
 }
 
-template <typename Tin, typename Tout, bool kTwoD>
+template <typename Tin, typename Tout, bool kTwoD, bool kZoh>
 __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
@@ -115,6 +115,7 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     __shared__ float s_dl2[kWave][kStride];               // Delta * log2 e
     __shared__ float s_du[kWave][kStride];                // Delta * u
     __shared__ float s_y[kTileWaves][kWave][kStride];     // per wave: its states' C h
+    __shared__ float s_u[kZoh ? kWave : 1][kStride];      // u itself (zero-order-hold B only)
 
     // XCD-aware numbering: hardware places workgroup i on XCD i % 8
     const int bid = blockIdx.x;
@@ -155,10 +156,11 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     // Scan role: lane = channel d0 + lane, states 4 wv .. 4 wv + 3.
     const int sd = d0 + lane < Dc ? d0 + lane : Dc - 1;
     const int sc = k * Dc + sd;
-    float an[4], h[4];
+    float an[4], h[4], inv_a[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         an[j] = A[static_cast<size_t>(sc) * N + 4 * wv + j];
+        inv_a[j] = kZoh ? 1.0f / an[j] : 0.0f;
         h[j] = 0.0f;
     }
     // the wave's four B and C rows: one base each, rows L elements apart
@@ -214,6 +216,7 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
                 const float dl = t + e >= tnew ? timescale(dv[e] + ld_bias, sp) : 0.0f;
                 s_dl2[lr][4 * lq + e] = dl * kLog2e;
                 s_du[lr][4 * lq + e] = dl * uv[e];
+                if constexpr (kZoh) s_u[lr][4 * lq + e] = uv[e];
                 skip[e] = ld_skip * uv[e];
             }
         }
@@ -244,11 +247,14 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
                 const int i = 8 * hh + e;
                 const float dl2 = s_dl2[lane][i];
                 const float du = s_du[lane][i];
+                const float ui = kZoh ? s_u[lane][i] : 0.0f;
                 float acc = 0.0f;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const float a = fast_exp2(dl2 * an[j]);
-                    h[j] = __builtin_fmaf(a, h[j], du * bq[j][e]);
+                    const float x2 = dl2 * an[j];
+                    const float a = fast_exp2(x2);
+                    const float q = kZoh ? zoh_q(x2, a, du, ui, inv_a[j]) : du;
+                    h[j] = __builtin_fmaf(a, h[j], q * bq[j][e]);
                     acc = __builtin_fmaf(cq[j][e], h[j], acc);
                 }
                 yp[i] = acc;
@@ -280,12 +286,12 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     }
 }
 
-template <typename Tin, typename Tout, bool kTwoD>
-vmb_status launch_tiles_impl(const ScanArgs& a, Tout* y, const void* xt) {
+template <typename Tin, typename Tout, bool kTwoD, bool kZoh>
+vmb_status launch_tiles_zoh(const ScanArgs& a, Tout* y, const void* xt) {
     const int n_cg = int((a.channels + kWave - 1) / kWave);
     const long long n_wg = static_cast<long long>(n_cg) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL((k_full_scan_tiles<Tin, Tout, kTwoD>), dim3(static_cast<unsigned>(n_wg)),
+    hipLaunchKernelGGL((k_full_scan_tiles<Tin, Tout, kTwoD, kZoh>), dim3(static_cast<unsigned>(n_wg)),
                        dim3(kTileThreads), 0, a.stream, static_cast<const Tin*>(a.u),
                        static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
                        static_cast<const Tin*>(a.C), a.D, a.dt_bias, y, static_cast<const Tin*>(xt),
@@ -294,7 +300,20 @@ vmb_status launch_tiles_impl(const ScanArgs& a, Tout* y, const void* xt) {
     return check_launch();
 }
 
+template <typename Tin, typename Tout, bool kTwoD>
+vmb_status launch_tiles_impl(const ScanArgs& a, Tout* y, const void* xt) {
+    return (a.options & VMB_SCAN_ZOH) ? launch_tiles_zoh<Tin, Tout, kTwoD, true>(a, y, xt)
+                                      : launch_tiles_zoh<Tin, Tout, kTwoD, false>(a, y, xt);
+}
+
 }  // namespace
+
+// Whether the tile kernel takes this shape at all (N = 16, whole tiles; bf16
+// rows of even length): the zero-order-hold option runs here whatever the
+// number of rows.
+bool tiles_take(const ScanArgs& a) {
+    return a.N == 16 && a.L >= kTP && !(a.in_dt == VMB_BF16 && (a.L % 2) != 0);
+}
 
 // Many channel rows (each sequence's channels split into 64-channel
 // workgroups still give several waves per SIMD), N = 16, L >= 16; bf16 rows

@@ -61,6 +61,22 @@ __device__ __forceinline__ float timescale(float v, bool softplus) {
     return __builtin_fmaxf(v, 0.0f) + log1p_unit(e);
 }
 
+// Zero-order-hold coefficient of B (eq. 4, second line read as
+// (Delta A)^-1 (exp(Delta A) - I) Delta B): Bbar u = q * B with
+// q = phi(x) Delta u, phi(x) = (e^x - 1) / x, x = Delta A. The caller passes
+// x2 = x log2(e) and a = exp2(x2), which it has for Abar, and inv_a = 1 / A.
+// Near x = 0, e^x - 1 cancels in binary32, so |x| < 0.02 takes phi's cubic
+// Taylor polynomial (truncation below 1.3e-9 relative) and larger |x| takes
+// (a - 1) u / A (the rounding of a then costs below 3e-6 relative).
+__device__ __forceinline__ float zoh_q(float x2, float a, float du, float u, float inv_a) {
+    constexpr float kLn2 = 0.69314718055994531f;
+    constexpr float c1 = kLn2 / 2.0f, c2 = kLn2 * kLn2 / 6.0f, c3 = kLn2 * kLn2 * kLn2 / 24.0f;
+    const float p = __builtin_fmaf(__builtin_fmaf(__builtin_fmaf(c3, x2, c2), x2, c1), x2, 1.0f);
+    const float near = p * du;
+    const float far = (a - 1.0f) * (inv_a * u);
+    return __builtin_fabsf(x2) < 0.02f * kLog2e ? near : far;
+}
+
 // Cross-scan position maps. Direction k reads pixel pix(k, t) at position t:
 //   k = 0: t                         k = 2: L - 1 - t
 //   k = 1: (t % H) * W + t / H       k = 3: same as 1 at L - 1 - t

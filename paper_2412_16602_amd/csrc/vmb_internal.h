@@ -151,6 +151,7 @@ bool use_chunked_full(const ScanArgs& a);
 // writes sequence-layout output to y_seq.
 constexpr int64_t kTilesMinRows = 16384;
 bool use_tiles_full(const ScanArgs& a);
+bool tiles_take(const ScanArgs& a);
 // The 2-D layout of that path also reads column-major copies of the input
 // planes (xt, written by launch_transpose_planes into the workspace after the
 // per-direction outputs), so directions 1 and 3 load contiguous rows.

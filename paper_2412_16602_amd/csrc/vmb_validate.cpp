@@ -128,11 +128,12 @@ vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
         if (a.K != 4 || a.H < 1 || a.W < 1 || prod({a.H, a.W}) != a.L) return VMB_ERR_SHAPE;
     }
     if (!supported_n(a.N)) return VMB_ERR_UNSUPPORTED;
-    const unsigned known =
-        VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST | VMB_MEAN_POOLED;
+    const unsigned known = VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST |
+                           VMB_MEAN_POOLED | VMB_SCAN_ZOH;
     if (a.options & ~known) return VMB_ERR_UNSUPPORTED;
+    if (!mean_variant && (a.options & ~static_cast<unsigned>(VMB_SCAN_ZOH))) return VMB_ERR_UNSUPPORTED;
     if ((a.options & VMB_MEAN_POOLED) && a.options != VMB_MEAN_POOLED) return VMB_ERR_UNSUPPORTED;
-    if (a.options && !mean_variant) return VMB_ERR_UNSUPPORTED;
+    if ((a.options & VMB_SCAN_ZOH) && (a.options & VMB_MEAN_RAW)) return VMB_ERR_UNSUPPORTED;
     const bool no_bcast = (a.options & VMB_MEAN_NO_BROADCAST) != 0;
     if (no_bcast && (a.layout != VMB_LAYOUT_SEQ || (a.options & VMB_MEAN_SKIP_PER_CHANNEL)))
         return VMB_ERR_UNSUPPORTED;

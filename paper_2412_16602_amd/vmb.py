@@ -24,6 +24,8 @@ VMB_F32, VMB_BF16 = 0, 1
 VMB_LAYOUT_SEQ, VMB_LAYOUT_2D = 0, 1
 # vmb_mean_option bits (vmb_mean_scan_fwd_ex)
 VMB_MEAN_SKIP_PER_CHANNEL, VMB_MEAN_RAW, VMB_MEAN_NO_BROADCAST, VMB_MEAN_POOLED = 1, 2, 4, 8
+# vmb_scan_option bits (vmb_selective_scan_fwd_ex; vmb_mean_scan_fwd_ex takes them too)
+VMB_SCAN_ZOH = 16
 
 STATUS = {0: "VMB_OK", 1: "VMB_ERR_NULL", 2: "VMB_ERR_SHAPE", 3: "VMB_ERR_DTYPE",
           4: "VMB_ERR_ALIGN", 5: "VMB_ERR_ALIAS", 6: "VMB_ERR_UNSUPPORTED",
@@ -59,8 +61,10 @@ def load_library():
         fn = getattr(lib, name)
         fn.argtypes = scan
         fn.restype = I
-    lib.vmb_mean_scan_fwd_ex.argtypes = scan[:-1] + [ctypes.c_uint, P]
-    lib.vmb_mean_scan_fwd_ex.restype = I
+    for name in ("vmb_selective_scan_fwd_ex", "vmb_mean_scan_fwd_ex"):
+        fn = getattr(lib, name)
+        fn.argtypes = scan[:-1] + [ctypes.c_uint, P]
+        fn.restype = I
     lib.vmb_discrete_scan.argtypes = [P, P, P, P, P, I64, I64, I64, P]
     lib.vmb_discrete_scan.restype = I
     lib.vmb_channel_mean.argtypes = [P, P, I64, I64, I64, P]
@@ -220,6 +224,13 @@ def vmb_selective_scan_fwd(u, delta, A, B, C, D, dt_bias, delta_softplus, y,
     """Full selective scan; shapes as in include/vmb.h. Returns y."""
     return _scan("vmb_selective_scan_fwd", False, u, delta, A, B, C, D, dt_bias, delta_softplus,
                  y, layout, workspace, stream)
+
+
+def vmb_selective_scan_fwd_ex(u, delta, A, B, C, D, dt_bias, delta_softplus, y, options: int,
+                              layout: int = VMB_LAYOUT_SEQ, workspace=None, stream=None):
+    """Full selective scan with options (VMB_SCAN_* bits). Returns y."""
+    return _scan("vmb_selective_scan_fwd_ex", False, u, delta, A, B, C, D, dt_bias,
+                 delta_softplus, y, layout, workspace, stream, options=options)
 
 
 def vmb_mean_scan_fwd(u, delta, A, B, C, D, dt_bias, delta_softplus, y,

@@ -86,8 +86,10 @@ def run_scan(inp: workloads.Inputs, variant: str, layout: str, out_dtype=None, s
     if options is not None and options & vmb.VMB_MEAN_NO_BROADCAST and layout == "seq":
         shape = shape[:2] + (1,) + shape[3:]
     y = torch.empty(shape, dtype=out_dtype, device=dev())
-    if options is not None:
-        assert variant == "mean"
+    if options is not None and variant == "full":
+        vmb.vmb_selective_scan_fwd_ex(u, dl, A, B, C, D, bias, softplus, y, options, layout=lay,
+                                      workspace=workspace)
+    elif options is not None:
         vmb.vmb_mean_scan_fwd_ex(u, dl, A, B, C, D, bias, softplus, y, options, layout=lay,
                                  workspace=workspace)
     else:
@@ -106,5 +108,5 @@ def oracle_seq(inp: workloads.Inputs, variant: str, layout: str, softplus=True, 
     args = (u, dl, inp.A, inp.B, inp.C, inp.D if use_d else None,
             inp.dt_bias if use_bias else None, softplus)
     if variant == "full":
-        return oracle.full_scan(*args, sel=sel)
+        return oracle.full_scan(*args, sel=sel, options=options)
     return oracle.mean_scan(*args, sel=sel, options=options)

@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) >= {"vmb_cross_scan", "vmb_cross_merge", "vmb_selective_scan_fwd",
                           "vmb_mean_scan_fwd", "vmb_scan_workspace_bytes", "vmb_status_string",
                           "vmb_abi_version", "vmb_discrete_scan", "vmb_channel_mean",
-                          "vmb_mean_scan_fwd_ex"}
+                          "vmb_mean_scan_fwd_ex", "vmb_selective_scan_fwd_ex"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -56,13 +56,13 @@ def scan_call(lib, fn="vmb_selective_scan_fwd", **kw):
     args = [a["u"], a["delta"], a["A"], a["B"], a["C"], a["D"], a["dt_bias"], a["sp"], a["y"],
             a["batch"], a["K"], a["channels"], a["L"], a["N"], a["in_dt"], a["out_dt"],
             a["layout"], a["H"], a["W"], a["ws"], a["ws_bytes"]]
-    if fn == "vmb_mean_scan_fwd_ex":
+    if fn in ("vmb_mean_scan_fwd_ex", "vmb_selective_scan_fwd_ex"):
         args.append(a.get("options", 0))
     return getattr(lib, fn)(*args, a["stream"])
 
 
 @pytest.mark.parametrize("fn", ["vmb_selective_scan_fwd", "vmb_mean_scan_fwd",
-                                "vmb_mean_scan_fwd_ex"])
+                                "vmb_mean_scan_fwd_ex", "vmb_selective_scan_fwd_ex"])
 @pytest.mark.parametrize("kw,expect", [
     (dict(u=None), NULL), (dict(delta=None), NULL), (dict(A=None), NULL), (dict(B=None), NULL),
     (dict(C=None), NULL), (dict(y=None), NULL),
@@ -94,13 +94,26 @@ def test_mean_options_rules(lib):
     passed = (OK, 8)
     for opt in (0, SKIP1, RAW, NOBC, SKIP1 | RAW, RAW | NOBC):
         assert scan_call(lib, ex, options=opt) in passed
-    assert scan_call(lib, ex, options=16) == UNSUP
+    assert scan_call(lib, ex, options=32) == UNSUP
     # the pooled reading only on its own, in either layout
     assert scan_call(lib, ex, options=POOL) in passed
     assert scan_call(lib, ex, options=POOL, layout=TWO_D) in passed
     for other in (SKIP1, RAW, NOBC):
         assert scan_call(lib, ex, options=POOL | other) == UNSUP
     assert scan_call(lib, ex, options=NOBC | SKIP1) == UNSUP
+    # the zero-order-hold B: with the main reading, D1 and no-broadcast, not with R2 or pooled
+    ZOH = vmb.VMB_SCAN_ZOH
+    assert "VMB_SCAN_ZOH = 16" in text and ZOH == 16
+    for opt in (ZOH, ZOH | SKIP1, ZOH | NOBC):
+        assert scan_call(lib, ex, options=opt) in passed
+    for opt in (ZOH | RAW, ZOH | POOL):
+        assert scan_call(lib, ex, options=opt) == UNSUP
+    full = "vmb_selective_scan_fwd_ex"
+    assert scan_call(lib, full, options=0) in passed
+    assert scan_call(lib, full, options=ZOH) in passed
+    assert scan_call(lib, full, options=ZOH, layout=TWO_D) in passed
+    for opt in (SKIP1, RAW, NOBC, POOL, 32):
+        assert scan_call(lib, full, options=opt) == UNSUP
     assert scan_call(lib, ex, options=NOBC, layout=TWO_D) == UNSUP
     assert scan_call(lib, ex, options=SKIP1 | RAW, layout=TWO_D) in passed
     # without the broadcast y holds batch*K*L elements: [P(7), +4*12*4 B) overlaps
