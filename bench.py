@@ -341,9 +341,10 @@ def table1_bench(steps: int, warmup: int):
 
 
 def variants_bench(steps: int, warmup: int):
-    """The mean scan's reading variants (vmb_mean_scan_fwd_ex options) at the
-    stage-1 workload, next to the main reading: µs per call, inputs rotated
-    past the MALL, events on the launch stream."""
+    """The mean scan's reading variants (vmb_mean_scan_fwd_ex options) and the
+    zero-order-hold B of both scans at the stage-1 workload, next to the main
+    reading: µs per call, inputs rotated past the MALL, events on the launch
+    stream."""
     import torch
 
     from paper_2412_16602_amd import vmb
@@ -354,7 +355,10 @@ def variants_bench(steps: int, warmup: int):
     opts = {"main": 0, "skip_per_channel": vmb.VMB_MEAN_SKIP_PER_CHANNEL, "raw": vmb.VMB_MEAN_RAW,
             "no_broadcast": vmb.VMB_MEAN_NO_BROADCAST,
             "raw_no_broadcast": vmb.VMB_MEAN_RAW | vmb.VMB_MEAN_NO_BROADCAST,
-            "pooled": vmb.VMB_MEAN_POOLED}
+            "pooled": vmb.VMB_MEAN_POOLED,
+            "zoh": vmb.VMB_SCAN_ZOH,
+            # the full scan, first-order and zero-order-hold B (no T)
+            "full_first_order": ("full", 0), "full_zoh": ("full", vmb.VMB_SCAN_ZOH)}
     rows = []
     for layout in ("seq", "2d"):
         inp = workloads.make_inputs(shape, layout)
@@ -364,26 +368,30 @@ def variants_bench(steps: int, warmup: int):
                     B=g(inp.B), C=g(inp.C), D=g(inp.D), dt_bias=g(inp.dt_bias))
         nbytes = ss2d_bytes(shape, shape.batch) if layout == "2d" else seq_bytes(shape, shape.batch)
         n = max(2, -(-ROTATE_BYTES // nbytes))
-        need = vmb.vmb_scan_workspace_bytes(True, shape.batch, 4, shape.channels, shape.L,
-                                            shape.N, lay)
+        need = max(vmb.vmb_scan_workspace_bytes(v, shape.batch, 4, shape.channels, shape.L,
+                                                shape.N, lay) for v in (0, 1))
         sets = [{k: (v.clone() if i else v) for k, v in base.items()} for i in range(n)]
         ws = torch.empty(need, dtype=torch.uint8, device=dev)
         for name, opt in opts.items():
-            if layout == "2d" and opt & vmb.VMB_MEAN_NO_BROADCAST:
+            full = isinstance(opt, tuple)
+            if full:
+                opt = opt[1]
+            if layout == "2d" and not full and opt & vmb.VMB_MEAN_NO_BROADCAST:
                 continue
             if layout == "2d":
                 yshape = tuple(inp.x.shape)
             else:
                 yshape = tuple(inp.delta.shape)
-                if opt & vmb.VMB_MEAN_NO_BROADCAST:
+                if not full and opt & vmb.VMB_MEAN_NO_BROADCAST:
                     yshape = yshape[:2] + (1,) + yshape[3:]
             ys = [torch.empty(yshape, device=dev) for _ in range(n)]
 
+            fn = vmb.vmb_selective_scan_fwd_ex if full else vmb.vmb_mean_scan_fwd_ex
+
             def call(i):
                 d = sets[i % n]
-                vmb.vmb_mean_scan_fwd_ex(d["u"], d["delta"], d["A"], d["B"], d["C"], d["D"],
-                                         d["dt_bias"], True, ys[i % n], opt, layout=lay,
-                                         workspace=ws, stream=stream)
+                fn(d["u"], d["delta"], d["A"], d["B"], d["C"], d["D"], d["dt_bias"], True,
+                   ys[i % n], opt, layout=lay, workspace=ws, stream=stream)
             for i in range(warmup):
                 call(i)
             torch.cuda.synchronize()
@@ -399,7 +407,8 @@ def variants_bench(steps: int, warmup: int):
             del ys
         del sets, ws
         torch.cuda.empty_cache()
-    return {"metric": "VMeanba reading variants, stage-1 56x56 c192 N16 fp32 (us/call)",
+    return {"metric": "VMeanba reading variants and zero-order-hold B, stage-1 56x56 c192 N16 fp32 "
+                      "(us/call)",
             "unit": "us/call", "dtype": "f32", "data": "synthetic", "rows": rows}
 
 

@@ -187,16 +187,21 @@ __device__ __forceinline__ void load_run_2d(const Tin* plane, int k, int t0, int
 // run aggregate, the inclusive scan over the wave, this wave's aggregate
 // published to xg[wv] by the last lane, and the lane's exclusive prefix
 // (Pex, Hex) kept for phase 2.
-template <int T, typename Tin>
+// With kZoh, Bbar u takes the zero-order-hold form (zoh_q, from the run's u
+// values uvr and inv_an = 1 / A_n) instead of Delta u.
+template <int T, typename Tin, bool kZoh = false>
 __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], const float (&du)[T],
                                              float s2, const Tin* bsrc, float (&a)[T],
                                              float (&bu)[T], float& Pex, float& Hex,
-                                             float (*xg)[2], int lane, int wv) {
+                                             float (*xg)[2], int lane, int wv,
+                                             const float (&uvr)[T], float inv_an) {
     float agg = 0.0f;
 #pragma unroll
     for (int i = 0; i < T; ++i) {
-        a[i] = fast_exp2(dl2[i] * an);
-        bu[i] = du[i] * to_f32(bsrc[i]);
+        const float x2 = dl2[i] * an;
+        a[i] = fast_exp2(x2);
+        const float q = kZoh ? zoh_q(x2, a[i], du[i], uvr[i], inv_an) : du[i];
+        bu[i] = q * to_f32(bsrc[i]);
         agg = __builtin_fmaf(a[i], agg, bu[i]);
     }
     float P = fast_exp2(s2 * an);
@@ -298,7 +303,7 @@ __device__ __forceinline__ void stage_one(const Tin* base, int p, int s, Tin* ds
 // LDS copies above) are done: vmcnt(0), other counters untouched.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
-template <int N, int T, int kWv, typename Tin, typename Tout, bool kTwoD>
+template <int N, int T, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh>
 __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
@@ -427,10 +432,13 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         auto pair_step = [&](int n0, Tin (*bcur)[kStageMax], Tin (*ccur)[kStageMax],
                              float (*xq)[kComputeWaves][2]) {
             const float2 a01 = *reinterpret_cast<const float2*>(an + n0);
+            const float inv0 = kZoh ? 1.0f / a01.x : 0.0f, inv1 = kZoh ? 1.0f / a01.y : 0.0f;
             float a0[T], bu0[T], a1[T], bu1[T];
             float Pex0, Hex0, Pex1, Hex1;
-            state_phase1<T>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0, xq[0], lane, wv);
-            state_phase1<T>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1, xq[1], lane, wv);
+            state_phase1<T, Tin, kZoh>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0,
+                                       xq[0], lane, wv, uv, inv0);
+            state_phase1<T, Tin, kZoh>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1,
+                                       xq[1], lane, wv, uv, inv1);
             __syncthreads();
             state_phase2<T, kWv>(a0, bu0, Pex0, Hex0, &ccur[0][run], yv, xq[0], &hcar[wv][n0], lane,
                                  g, w);
@@ -469,7 +477,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
 
 // Chunked full scan: picks the run length and waves per channel from L.
 namespace {
-template <int N, int kWv, typename Tin, typename Tout, bool kTwoD>
+template <int N, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh>
 vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y) {
     constexpr int T = 13;  // positions per lane run
     constexpr int G = kComputeWaves / kWv;  // channels per workgroup
@@ -477,7 +485,7 @@ vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y) {
     const long long n_wg = static_cast<long long>(n_groups) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
     const dim3 grid(static_cast<unsigned>(n_wg)), block(kStageThreads);
-    hipLaunchKernelGGL((k_full_scan_chunked<N, T, kWv, Tin, Tout, kTwoD>), grid, block, 0, a.stream,
+    hipLaunchKernelGGL((k_full_scan_chunked<N, T, kWv, Tin, Tout, kTwoD, kZoh>), grid, block, 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,
                        y, int(a.K), int(a.channels), int(a.L), int(a.H), int(a.W), a.softplus,
@@ -487,12 +495,18 @@ vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y) {
 
 // Waves per channel from L: cover the sequence in one chunk where possible
 // (runs of 13 positions, 64 lanes per wave).
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kZoh>
+vmb_status launch_chunked_waves(const ScanArgs& a, Tout* y) {
+    const int64_t L = a.L;
+    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD, kZoh>(a, y);
+    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD, kZoh>(a, y);
+    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD, kZoh>(a, y);
+}
+
 template <int N, typename Tin, typename Tout, bool kTwoD>
 vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y) {
-    const int64_t L = a.L;
-    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD>(a, y);
-    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD>(a, y);
-    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD>(a, y);
+    return (a.options & VMB_SCAN_ZOH) ? launch_chunked_waves<N, Tin, Tout, kTwoD, true>(a, y)
+                                      : launch_chunked_waves<N, Tin, Tout, kTwoD, false>(a, y);
 }
 }  // namespace
 

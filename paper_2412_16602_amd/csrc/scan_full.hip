@@ -113,11 +113,12 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L > kShortMaxL; }
 
 vmb_status launch_full_scan(const ScanArgs& a) {
-    // the zero-order-hold B runs in the tile kernel (N = 16) or the lane
-    // kernel (other shapes) only
+    // the zero-order-hold B runs in the tile, positions-over-lanes and lane
+    // kernels (not the short-sequence one: those shapes take the tile kernel)
     const bool zoh = (a.options & VMB_SCAN_ZOH) != 0;
-    const bool tiles = zoh ? tiles_take(a) : use_tiles_full(a);
-    if (tiles || (!zoh && (use_chunked_full(a) || use_short_full(a)))) {
+    const bool tiles =
+        use_tiles_full(a) || (zoh && !use_chunked_full(a) && tiles_take(a));
+    if (tiles || use_chunked_full(a) || (!zoh && use_short_full(a))) {
         auto run = [&](void* y_seq, const void* xt) {
             if (tiles) return launch_full_tiles(a, y_seq, xt);
             return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq);

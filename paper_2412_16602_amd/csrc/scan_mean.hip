@@ -121,16 +121,23 @@ __device__ __forceinline__ void store_reduced(float yt, Tout* __restrict__ y,
 // blockIdx.y)): every wave's partial sums over its channels, for the lanes'
 // positions, left in part[wv][0..N+2) (exp sums per state, s, r).
 // A wave's partial sums fill N + 2 rows (exp sums per state, s, r), one more
-// (the input sum) when T averages the raw terms.
-template <int N, typename Tin, bool kTwoD, bool kRaw>
+// (the input sum) when T averages the raw terms, N more (the sums of the
+// zero-order-hold terms phi(Delta A_n) Delta u, rows N + 2 ..) with kZoh.
+template <int N, bool kRaw, bool kZoh>
+constexpr int part_rows() {
+    return N + 2 + (kRaw ? 1 : 0) + (kZoh ? N : 0);
+}
+
+template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh = false>
 __device__ __forceinline__ void reduce_partials(
-    float (*part)[N + 2 + int(kRaw)][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
+    float (*part)[(part_rows<N, kRaw, kZoh>())][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
     const float* __restrict__ A, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, int K, int Dc, int L, int H, int W, int C, int softplus) {
     // Each wave's slice part[wv] first holds its channel parameters (two
-    // buffers of kAhead rows: A[c, 0..N) log2(e), dt_bias[c], D[c]), read back as
-    // wave-uniform broadcasts, and afterwards its partial sums.
-    constexpr int kPS = (N + 2 + 3) & ~3;  // parameter row stride (16-byte rows)
+    // buffers of kAhead rows: A[c, 0..N) log2(e), dt_bias[c], D[c], and with
+    // kZoh 1 / A[c, 0..N)), read back as wave-uniform broadcasts, and
+    // afterwards its partial sums.
+    constexpr int kPS = (N + 2 + (kZoh ? N : 0) + 3) & ~3;  // parameter row stride (16-byte rows)
     static_assert(2 * kAhead * kPS <= (N + 2) * kC, "parameter buffers fit a wave's slice");
     static_assert(kAhead <= 32, "parameter row layout");
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
@@ -150,9 +157,11 @@ __device__ __forceinline__ void reduce_partials(
     // byte offsets of this lane within a row (32-bit, non-negative)
     const unsigned toff = static_cast<unsigned>(tc) * sizeof(Tin);
     const unsigned soff = static_cast<unsigned>(src) * sizeof(Tin);
-    float acc[N];
+    float acc[N], zacc[kZoh ? N : 1];
 #pragma unroll
     for (int n = 0; n < N; ++n) acc[n] = 0.0f;
+#pragma unroll
+    for (int n = 0; n < (kZoh ? N : 1); ++n) zacc[n] = 0.0f;
     float s = 0.0f, r = 0.0f, q = 0.0f;
     const int d0 = (wv * Dc) / kRedWaves, d1 = ((wv + 1) * Dc) / kRedWaves;
     const int nw = d1 - d0;  // channels of this wave
@@ -193,7 +202,10 @@ __device__ __forceinline__ void reduce_partials(
 #pragma unroll
         for (int m = 0; m < kPA; ++m) {
             const int idx = lane + m * kC;
-            if (idx < kAhead * N) base[(idx / N) * kPS + idx % N] = pa[m] * kLog2e;
+            if (idx < kAhead * N) {
+                base[(idx / N) * kPS + idx % N] = pa[m] * kLog2e;
+                if constexpr (kZoh) base[(idx / N) * kPS + N + 2 + idx % N] = 1.0f / pa[m];
+            }
         }
         if (lane < kAhead) base[lane * kPS + N] = pbd;
         else if (lane >= 32 && lane < 32 + kAhead) base[(lane - 32) * kPS + N + 1] = pbd;
@@ -205,9 +217,25 @@ __device__ __forceinline__ void reduce_partials(
         bias = row[N];
         dskip = row[N + 1];
     };
-    auto channel = [&](const float (&an)[N], float bias, float dskip, float dv, float uv) {
+    // 1 / A of the same channel (kZoh)
+    auto read_inv = [&](int buf, int i, int n) {
+        return prm[buf * kAhead * kPS + i * kPS + N + 2 + n];
+    };
+    auto channel = [&](const float (&an)[N], float bias, float dskip, float dv, float uv, int buf,
+                       int i) {
         const float dl = valid ? timescale(dv + bias, sp) : 0.0f;
-        if constexpr (kRaw) {
+        if constexpr (kZoh) {
+            // means of exp(Delta A_n) and of the zero-order-hold terms per state
+            const float du = dl * uv;
+#pragma unroll
+            for (int n = 0; n < N; ++n) {
+                const float x2 = dl * an[n];  // an = A log2(e)
+                const float a = fast_exp2(x2);
+                acc[n] += a;
+                zacc[n] += zoh_q(x2, a, du, uv, read_inv(buf, i, n));
+            }
+            s = __builtin_fmaf(dl, uv, s);
+        } else if constexpr (kRaw) {
             // sums of A log2(e) (the same in every lane), Delta and u
 #pragma unroll
             for (int n = 0; n < N; ++n) acc[n] += an[n];
@@ -223,6 +251,10 @@ __device__ __forceinline__ void reduce_partials(
         // would keep every channel's parameters live)
 #pragma unroll
         for (int n = 0; n < N; ++n) asm volatile("" : "+v"(acc[n]));
+        if constexpr (kZoh) {
+#pragma unroll
+            for (int n = 0; n < N; ++n) asm volatile("" : "+v"(zacc[n]));
+        }
         if constexpr (kRaw)
             asm volatile("" : "+v"(s), "+v"(r), "+v"(q));
         else
@@ -253,7 +285,7 @@ __device__ __forceinline__ void reduce_partials(
                 __builtin_amdgcn_sched_barrier(0);
                 float an[N], bias, dskip;
                 read_par(buf, j, an, bias, dskip);
-                channel(an, bias, dskip, dv[j], uv[j]);
+                channel(an, bias, dskip, dv[j], uv[j], buf, j);
                 load_ch(i0 + kAhead + j, dv[j], uv[j]);
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -265,7 +297,7 @@ __device__ __forceinline__ void reduce_partials(
             if (j < rem) {
                 float an[N], bias, dskip;
                 read_par(nb & 1, j, an, bias, dskip);
-                channel(an, bias, dskip, dv[j], uv[j]);
+                channel(an, bias, dskip, dv[j], uv[j], nb & 1, j);
             }
         }
     }
@@ -274,18 +306,24 @@ __device__ __forceinline__ void reduce_partials(
     part[wv][N][lane] = s;
     part[wv][N + 1][lane] = r;
     if constexpr (kRaw) part[wv][N + 2][lane] = q;
+    if constexpr (kZoh) {
+#pragma unroll
+        for (int n = 0; n < N; ++n) part[wv][N + 2 + n][lane] = zacc[n];
+    }
 }
 
 // The pair (a, b) of state n at one position from the channel-group sums:
 // the means of the discretised terms, (mean exp(Delta A), B mean(Delta u)),
 // or with kRaw the discretisation of the means, (exp(mean Delta mean A),
 // mean Delta B mean u).
-template <int N, bool kRaw>
-__device__ __forceinline__ void reduced_pair(const float (*part)[N + 2 + int(kRaw)][kC], int n,
-                                             int lane, float inv, float bval, float& a,
+template <int N, bool kRaw, bool kZoh = false>
+__device__ __forceinline__ void reduced_pair(const float (*part)[(part_rows<N, kRaw, kZoh>())][kC],
+                                             int n, int lane, float inv, float bval, float& a,
                                              float& bb) {
     float sm = 0.0f, am = 0.0f;
-    for (int w = 0; w < kRedWaves; ++w) sm += part[w][N][lane];
+    // zero-order hold: the state's own mean of phi(Delta A_n) Delta u
+    const int srow = kZoh ? N + 2 + n : N;
+    for (int w = 0; w < kRedWaves; ++w) sm += part[w][srow][lane];
     for (int w = 0; w < kRedWaves; ++w) am += part[w][n][lane];
     sm *= inv;
     am *= inv;
@@ -301,15 +339,15 @@ __device__ __forceinline__ void reduced_pair(const float (*part)[N + 2 + int(kRa
     }
 }
 
-template <int N, typename Tin, bool kTwoD, bool kRaw>
+template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh>
 __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
     int softplus) {
-    __shared__ __align__(16) float part[kRedWaves][N + 2 + int(kRaw)][kC];
-    reduce_partials<N, Tin, kTwoD, kRaw>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
-                                         softplus);
+    __shared__ __align__(16) float part[kRedWaves][(part_rows<N, kRaw, kZoh>())][kC];
+    reduce_partials<N, Tin, kTwoD, kRaw, kZoh>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
+                                               softplus);
     __syncthreads();
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
@@ -331,7 +369,7 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     float* agg_bk = ws.agg + bk * N * nchunks * 2;
     for (int n = wv; n < N; n += kRedWaves) {
         float a, bb;
-        reduced_pair<N, kRaw>(part, n, lane, inv, to_f32(Bm[(bk * N + n) * L + tc]), a, bb);
+        reduced_pair<N, kRaw, kZoh>(part, n, lane, inv, to_f32(Bm[(bk * N + n) * L + tc]), a, bb);
         // positions past the end act as the identity (1, 0)
         a = valid ? a : 1.0f;
         bb = valid ? bb : 0.0f;
@@ -807,7 +845,7 @@ vmb_status run_pooled(const ScanArgs& a) {
     return check_launch();
 }
 
-template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw>
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw, bool kZoh>
 vmb_status run(const ScanArgs& a) {
     const size_t bkn = static_cast<size_t>(a.batch * a.K);
     const MeanWsLayout lay = mean_ws_layout(a.batch, a.K, a.channels, a.L, N, kTwoD);
@@ -827,7 +865,9 @@ vmb_status run(const ScanArgs& a) {
     // rounds of workgroups, time spent waiting for an earlier chunk would
     // hold a compute unit that the separate passes keep busy.
     const long long wgs = static_cast<long long>(nchunks) * a.K * a.batch;
-    const bool fused = C == kC && nchunks <= kWave && (nchunks == 1 || wgs <= kFusedMaxGrid);
+    // (the zero-order-hold sums need more LDS than the one-launch kernel has
+    // room for next to its other buffers: those calls take the three passes)
+    const bool fused = !kZoh && C == kC && nchunks <= kWave && (nchunks == 1 || wgs <= kFusedMaxGrid);
     const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
     // 2-D layout: column-major copies of the planes first, so that every
     // direction's reduce reads stay coalesced
@@ -841,7 +881,7 @@ vmb_status run(const ScanArgs& a) {
     StoreOpts so;
     so.skip_own = (a.options & VMB_MEAN_SKIP_PER_CHANNEL) ? 1 : 0;
     so.no_bcast = (a.options & VMB_MEAN_NO_BROADCAST) ? 1 : 0;
-    if (fused) {
+    if constexpr (!kZoh) if (fused) {
         hipLaunchKernelGGL((k_mean_fused<N, Tin, Tout, kTwoD, kRaw>), grid, dim3(kC * kRedWaves),
                            0, a.stream, static_cast<const Tin*>(a.u),
                            static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
@@ -852,7 +892,7 @@ vmb_status run(const ScanArgs& a) {
         if (sf != VMB_OK || !kTwoD) return sf;
         return launch_merge_broadcast<Tin, Tout>(ws.ytil, a);
     }
-    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD, kRaw>), grid, dim3(kC * kRedWaves), 0,
+    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD, kRaw, kZoh>), grid, dim3(kC * kRedWaves), 0,
                        a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), a.D, a.dt_bias, xt, ws, K, Dc, L, H, W, C,
@@ -884,10 +924,10 @@ vmb_status run(const ScanArgs& a) {
     return launch_merge_broadcast<Tin, Tout>(ws.ytil, a);
 }
 
-template <int N, typename Tin, typename Tout, bool kRaw>
+template <int N, typename Tin, typename Tout, bool kRaw, bool kZoh = false>
 vmb_status dispatch_layout(const ScanArgs& a) {
-    return a.layout == VMB_LAYOUT_SEQ ? run<N, Tin, Tout, false, kRaw>(a)
-                                      : run<N, Tin, Tout, true, kRaw>(a);
+    return a.layout == VMB_LAYOUT_SEQ ? run<N, Tin, Tout, false, kRaw, kZoh>(a)
+                                      : run<N, Tin, Tout, true, kRaw, kZoh>(a);
 }
 
 template <int N, typename Tin, typename Tout>
@@ -895,6 +935,7 @@ vmb_status dispatch_reading(const ScanArgs& a) {
     if (a.options & VMB_MEAN_POOLED)
         return a.layout == VMB_LAYOUT_SEQ ? run_pooled<N, Tin, Tout, false>(a)
                                           : run_pooled<N, Tin, Tout, true>(a);
+    if (a.options & VMB_SCAN_ZOH) return dispatch_layout<N, Tin, Tout, false, true>(a);
     return (a.options & VMB_MEAN_RAW) ? dispatch_layout<N, Tin, Tout, true>(a)
                                       : dispatch_layout<N, Tin, Tout, false>(a);
 }

@@ -82,3 +82,75 @@ def test_2d(H, W, c, N):
     ref, scale = merged_oracle(inp, "full", options=ORA_ZOH)
     assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
                  what=f"zoh 2d {H}x{W}")
+
+
+# ---------------------------------------------------------------- under the mean (T of eq. 9)
+
+MEAN_CASES = [
+    ("b2_c24_L100_n16", dict(b=2, H=10, W=10, c=24, N=16)),
+    ("b1_c7_L200_n4", dict(b=1, H=8, W=25, c=7, N=4)),
+    ("b1_c5_L4500_n16", dict(b=1, H=1, W=4500, c=5, N=16)),  # 71 chunks: carry pass
+    ("b3_c3_L9_n1", dict(b=3, H=3, W=3, c=3, N=1)),
+]
+MEAN_OPTS = {"main": (0, 0),
+             "skip1": (vmb.VMB_MEAN_SKIP_PER_CHANNEL, oracle.MEAN_SKIP_PER_CHANNEL),
+             "nobc": (vmb.VMB_MEAN_NO_BROADCAST, oracle.MEAN_NO_BROADCAST)}
+
+
+@pytest.mark.parametrize("opt", list(MEAN_OPTS))
+@pytest.mark.parametrize("name,kw", MEAN_CASES, ids=[c[0] for c in MEAN_CASES])
+def test_mean_seq(name, kw, opt):
+    log(f"zoh mean seq {name} {opt}")
+    inp = inputs(layout="seq", seed=7 + len(name), **kw)
+    lib_o, ora_o = MEAN_OPTS[opt]
+    got = to_f64(run_scan(inp, "mean", "seq", options=LIB_ZOH | lib_o))
+    ref = oracle_seq(inp, "mean", "seq", options=ORA_ZOH | ora_o)
+    assert_close(got, ref, **FP32_TOL, what=f"zoh mean {name} {opt}")
+
+
+def test_mean_bf16():
+    log("zoh mean seq bf16")
+    inp = inputs(2, 8, 12, 20, 16, dtype="bf16", seed=31)
+    y = run_scan(inp, "mean", "seq", options=LIB_ZOH)
+    ref = oracle_seq(inp, "mean", "seq", options=ORA_ZOH)
+    assert_close(to_f64(y), ref, **BF16_TOL, what="zoh mean bf16")
+
+
+@pytest.mark.parametrize("H,W,c,N", [(7, 7, 32, 4), (12, 10, 24, 16)])
+def test_mean_2d(H, W, c, N):
+    log(f"zoh mean 2d {H}x{W}")
+    inp = inputs(2, H, W, c, N, layout="2d", seed=H + W)
+    got = to_f64(run_scan(inp, "mean", "2d", options=LIB_ZOH))
+    ref, scale = merged_oracle(inp, "mean", options=ORA_ZOH)
+    assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
+                 what=f"zoh mean 2d {H}x{W}")
+
+
+# positions-over-lanes kernel (N = 16, L > 416, few rows): 1, 2 and 4 waves per
+# channel, several chunks (L > 3328)
+CHUNKED = [("chunked_L500", dict(b=1, H=20, W=25, c=6, N=16)),
+           ("chunked_L1000", dict(b=1, H=25, W=40, c=5, N=16)),
+           ("chunked_L3136", dict(b=1, H=56, W=56, c=12, N=16)),
+           ("chunked_L4000", dict(b=1, H=40, W=100, c=3, N=16))]
+
+
+@pytest.mark.parametrize("name,kw", CHUNKED, ids=[c[0] for c in CHUNKED])
+def test_chunked_seq(name, kw):
+    log(f"zoh full {name}")
+    inp = inputs(layout="seq", seed=11 + len(name), **kw)
+    got = to_f64(run_scan(inp, "full", "seq", options=LIB_ZOH))
+    ref = oracle_seq(inp, "full", "seq", options=ORA_ZOH)
+    assert_close(got, ref, **FP32_TOL, what=f"zoh {name}")
+
+
+def test_chunked_bf16_and_2d():
+    log("zoh full chunked bf16 seq, f32 2-D")
+    inp = inputs(1, 28, 28, 8, 16, dtype="bf16", seed=21)
+    y = run_scan(inp, "full", "seq", options=LIB_ZOH)
+    ref = oracle_seq(inp, "full", "seq", options=ORA_ZOH)
+    assert_close(to_f64(y), ref, **BF16_TOL, what="zoh chunked bf16")
+    inp = inputs(1, 30, 30, 6, 16, layout="2d", seed=22)
+    got = to_f64(run_scan(inp, "full", "2d", options=LIB_ZOH))
+    ref, scale = merged_oracle(inp, "full", options=ORA_ZOH)
+    assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
+                 what="zoh chunked 2d")
