@@ -181,6 +181,34 @@ def mean_scan_pooled(u, delta, A, B, C, D=None, dt_bias=None, softplus=True,
     return y
 
 
+def projections(u, W, W_dt=None, N: int = 16):
+    """Selection projections of eq. 6 (Linear_N for B and C, Linear then the
+    channel expansion for the timescale), fp64, per direction k:
+      x_dbl[b,k,r,t] = sum_d W[k,r,d] u[b,k,d,t]          (R + 2N rows)
+      B = x_dbl[:, :, R:R+N],  C = x_dbl[:, :, R+N:R+2N]
+      delta[b,k,d,t] = sum_r W_dt[k,d,r] x_dbl[b,k,r,t]   (W_dt None, R = 1:
+                       x_dbl[b,k,0,t] for every d, the broadcast of eq. 6)
+    u [batch, K, Dc, L]; W [K, R+2N, Dc]; W_dt [K, Dc, R] or None.
+    Returns (delta, B, C) as float64 arrays. Each product is numpy's matmul.
+    """
+    u = np.asarray(u, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    batch, K, Dc, L = u.shape
+    R = W.shape[1] - 2 * N
+    assert W.shape == (K, R + 2 * N, Dc) and R >= 1
+    x_dbl = np.matmul(W[None], u)                     # [batch, K, R+2N, L]
+    B = x_dbl[:, :, R:R + N]
+    C = x_dbl[:, :, R + N:R + 2 * N]
+    if W_dt is None:
+        assert R == 1
+        delta = np.broadcast_to(x_dbl[:, :, :1], (batch, K, Dc, L)).copy()
+    else:
+        W_dt = np.asarray(W_dt, dtype=np.float64)
+        assert W_dt.shape == (K, Dc, R)
+        delta = np.matmul(W_dt[None], x_dbl[:, :, :R])  # [batch, K, Dc, L]
+    return delta, np.ascontiguousarray(B), np.ascontiguousarray(C)
+
+
 def discrete_scan(abar, bu, C, skip=None, nthreads: int = 0) -> np.ndarray:
     """One-state scan on materialised inputs in fp64.
 

@@ -745,3 +745,56 @@ def test_zoh_mean_is_channel_mean_of_full_when_timescale_shared():
                           True, options=oracle.ZOH)
     ref = np.broadcast_to(yf.mean(axis=2, keepdims=True), yf.shape)
     np.testing.assert_allclose(ym, ref, rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- selection projections (eq. 6)
+
+def test_projections_brute_force():
+    """Triple loops on a tiny case: x_dbl = W u per direction, B and C its rows
+    R.. and R+N.., delta the rank-R expansion of its first R rows."""
+    rng = np.random.default_rng(60)
+    batch, K, Dc, L, N, R = 2, 3, 4, 5, 2, 3
+    u = rng.standard_normal((batch, K, Dc, L)).astype(np.float32)
+    pw = workloads.make_projection_weights(K, Dc, N, R, seed=61)
+    delta, B, C = oracle.projections(u, pw.W, pw.W_dt, N=N)
+    for b in range(batch):
+        for k in range(K):
+            for t in range(L):
+                xd = [sum(float(pw.W[k, r, d]) * float(u[b, k, d, t]) for d in range(Dc))
+                      for r in range(R + 2 * N)]
+                for n in range(N):
+                    assert abs(B[b, k, n, t] - xd[R + n]) < 1e-12
+                    assert abs(C[b, k, n, t] - xd[R + N + n]) < 1e-12
+                for d in range(Dc):
+                    ref = sum(float(pw.W_dt[k, d, r]) * xd[r] for r in range(R))
+                    assert abs(delta[b, k, d, t] - ref) < 1e-12
+
+
+def test_projections_one_hot_input_reads_weight_columns():
+    """u = e_j at one position: B, C there are column j of W's B and C rows,
+    and zero elsewhere (a transposed W fails this)."""
+    K, Dc, L, N, R = 2, 6, 4, 3, 2
+    pw = workloads.make_projection_weights(K, Dc, N, R, seed=62)
+    u = np.zeros((1, K, Dc, L), np.float32)
+    u[0, 1, 4, 2] = 1.0
+    delta, B, C = oracle.projections(u, pw.W, pw.W_dt, N=N)
+    np.testing.assert_array_equal(B[0, 1, :, 2], pw.W[1, R:R + N, 4].astype(np.float64))
+    np.testing.assert_array_equal(C[0, 1, :, 2], pw.W[1, R + N:, 4].astype(np.float64))
+    mask = np.ones(L, bool)
+    mask[2] = False
+    assert not B[0, 1][:, mask].any() and not B[0, 0].any()
+    ref = pw.W_dt[1].astype(np.float64) @ pw.W[1, :R, 4].astype(np.float64)
+    np.testing.assert_allclose(delta[0, 1, :, 2], ref, rtol=1e-15, atol=0)
+
+
+def test_projections_broadcast_timescale():
+    """R = 1 without W_dt (Broadcast_D(Linear_1(u)) of eq. 6): delta is the
+    same for every channel and equals the single timescale row of W times u."""
+    rng = np.random.default_rng(63)
+    u = rng.standard_normal((1, 2, 5, 7)).astype(np.float32)
+    pw = workloads.make_projection_weights(2, 5, 4, 1, seed=64, broadcast=True)
+    delta, _, _ = oracle.projections(u, pw.W, None, N=4)
+    for k in range(2):
+        ref = pw.W[k, 0].astype(np.float64) @ u[0, k].astype(np.float64)
+        for d in range(5):
+            np.testing.assert_allclose(delta[0, k, d], ref, rtol=1e-14, atol=1e-15)

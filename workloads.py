@@ -194,3 +194,28 @@ def make_discrete_inputs(batch: int, channels: int, L: int, seed: int,
     C = rng.standard_normal((batch, L), dtype=np.float32)
     skip = rng.standard_normal((batch, channels, L), dtype=np.float32) if with_skip else None
     return DiscreteInputs(abar=abar, bu=bu, C=C, skip=skip)
+
+
+# ------------------------------------------------ selection projections (eq. 6)
+@dataclasses.dataclass
+class ProjectionWeights:
+    W: np.ndarray               # [K, R + 2N, channels]: R timescale rows, N rows for B, N for C
+    W_dt: Optional[np.ndarray]  # [K, channels, R], or None for the broadcast (R = 1)
+
+
+def make_projection_weights(K: int, channels: int, N: int, R: int, seed: int,
+                            broadcast: bool = False) -> ProjectionWeights:
+    """Random projection weights of the shapes eq. 6 implies, drawn directly
+    (PCG64, float32; W then W_dt): W ~ N(0, 1/channels) (unit-variance
+    outputs for unit-variance inputs), W_dt ~ N(0, 1/R). ``broadcast`` (R = 1)
+    leaves W_dt out: the timescale projection is Broadcast_D(Linear_1(u))."""
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((K, R + 2 * N, channels), dtype=np.float32)
+         * np.float32(1.0 / math.sqrt(channels))).astype(np.float32)
+    W_dt = None
+    if not broadcast:
+        W_dt = (rng.standard_normal((K, channels, R), dtype=np.float32)
+                * np.float32(1.0 / math.sqrt(R))).astype(np.float32)
+    else:
+        assert R == 1
+    return ProjectionWeights(W=W, W_dt=W_dt)
