@@ -58,6 +58,7 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2412_16602_amd", "csrc", f)
 METRIC = ("SS2D selective-scan µs/call + HBM GB/s (% peak), full vs mean, "
           "VMamba-T 56×56")
 ROTATE_BYTES = 768 << 20  # > 2x the 256 MB MALL
+MFMA_F32_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak
 
 
 def seq_bytes(s: workloads.Shape, batch: int, esz_in=4, esz_out=4) -> int:
@@ -504,6 +505,71 @@ def workloads_bench(steps: int, warmup: int):
             "rows": rows}
 
 
+def projections_bench(steps: int, warmup: int):
+    """The selection projections of eq. 6 (vmb_ss2d_projections) at every
+    N = 16 workload, in the scan's SEQ layout: the paper's broadcast timescale
+    (R = 1, Linear_1) and VMamba's rank ceil(channels / 32). us per call with
+    HIP events on the launch stream, enough input sets in turn that each call
+    reads u from HBM; algorithmic bytes are u read plus delta, B and C
+    written (the weights stay in cache), flops the two contractions."""
+    import torch
+
+    from paper_2412_16602_amd import vmb
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device=dev)
+    g.manual_seed(3)
+    rows = []
+    for shp in (workloads.STAGE1, workloads.STAGE2, workloads.STAGE3, workloads.STAGE4,
+                workloads.BATCHED_BF16, workloads.HIRES):
+        b, K, Dc, L, N = shp.batch, 4, shp.channels, shp.L, shp.N
+        dt = torch.bfloat16 if shp.dtype == "bf16" else torch.float32
+        esz = 2 if shp.dtype == "bf16" else 4
+        nbytes = b * K * L * (2 * Dc + 2 * N) * esz
+        n_sets = max(1, min(8, -(-ROTATE_BYTES // nbytes)))
+        us_in = [(torch.randn(b, K, Dc, L, device=dev, generator=g)).to(dt) for _ in range(n_sets)]
+        delta = torch.empty(b, K, Dc, L, device=dev, dtype=dt)
+        Bm = torch.empty(b, K, N, L, device=dev, dtype=dt)
+        Cm = torch.empty_like(Bm)
+        for R, bcast in ((1, True), (-(-Dc // 32), False)):
+            W = torch.randn(K, R + 2 * N, Dc, device=dev, generator=g) / math.sqrt(Dc)
+            Wdt = None if bcast else torch.randn(K, Dc, R, device=dev, generator=g) / math.sqrt(R)
+
+            def call(i):
+                vmb.vmb_ss2d_projections(us_in[i % n_sets], W, Wdt, delta, Bm, Cm, stream=stream)
+            for i in range(warmup):
+                call(i)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call(0)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            n = max(3, min(steps, int(0.2e6 / max(1.0, e0.elapsed_time(e1) * 1e3))))
+            e0.record(stream)
+            for i in range(n):
+                call(i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / n
+            flops = 2 * b * K * L * Dc * ((R + 2 * N) + (0 if bcast else R))
+            rows.append({"workload": shp.name, "dtype": shp.dtype, "R": R,
+                         "timescale": "broadcast" if bcast else "low-rank", "us": round(us, 2),
+                         "calls": n, "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                         "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                         "tflops": round(flops / (us * 1e-6) / 1e12, 2),
+                         "mfma_f32_frac": round(flops / (us * 1e-6) / 1e12 / MFMA_F32_PEAK_TFLOPS,
+                                                4)})
+        del us_in, delta, Bm, Cm
+        torch.cuda.empty_cache()
+    return {"metric": "selection projections of eq. 6, every N=16 workload (us/call)",
+            "unit": "us/call", "data": "synthetic",
+            "timing": "HIP events on the launch stream around consecutive calls",
+            "rows": rows}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -530,6 +596,9 @@ def main():
     ap.add_argument("--workloads", action="store_true",
                     help="after the main line, print a line timing the full and mean scans "
                          "at every N=16 workload, both layouts")
+    ap.add_argument("--projections", action="store_true",
+                    help="after the main line, print a line timing the selection projections "
+                         "of eq. 6 at every N=16 workload")
     ap.add_argument("--table1", action="store_true",
                     help="after the main line, print a second JSON line: the one-state scan "
                          "on materialised inputs at the paper's Table 1 shapes")
@@ -595,6 +664,8 @@ def main():
         print(json.dumps(variants_bench(args.steps, args.warmup)), flush=True)
     if args.workloads:
         print(json.dumps(workloads_bench(args.steps, 3)), flush=True)
+    if args.projections:
+        print(json.dumps(projections_bench(args.steps, 3)), flush=True)
     if args.table1:
         print(json.dumps(table1_bench(max(5, args.steps // 10), 3)), flush=True)
 

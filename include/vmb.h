@@ -283,6 +283,39 @@ vmb_status vmb_channel_mean(const float* x, float* xm, int64_t batch, int64_t ch
 size_t vmb_scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                                 int64_t L, int64_t N, vmb_layout layout);
 
+/*
+ * The selection projections of eq. 6 (Appendix A, Mamba paragraph), which
+ * make the scan's B, C and timescale functions of its input: per (b, k)
+ * sequence u[b,k,:,t] and with the direction's weights
+ * W[k] = [R timescale rows; N rows for B; N rows for C] over the channels,
+ *   x_dbl[r,t]       = sum_d W[k,r,d] u[b,k,d,t]          (r < R + 2N)
+ *   B[b,k,n,t]       = x_dbl[R + n, t]                     (s_B = Linear_N)
+ *   C[b,k,n,t]       = x_dbl[R + N + n, t]                 (s_C = Linear_N)
+ *   delta[b,k,d,t]   = sum_r W_dt[k,d,r] x_dbl[r,t]        (s_Delta, rank R)
+ * With W_dt NULL and R = 1, delta[b,k,d,t] = x_dbl[0,t] for every d: the
+ * paper's Broadcast_D(Linear_1(u)). delta is s_Delta(u): the scan entry
+ * points add the Parameter (dt_bias) and apply softplus. Products are
+ * accumulated in binary32 on the matrix cores.
+ *
+ *   u      : [batch, K, channels, L] (SEQ layout), dtype
+ *   W      : float32, [K, R + 2N, channels]
+ *   W_dt   : float32, [K, channels, R], or NULL (then R must be 1)
+ *   delta  : [batch, K, channels, L] (output), dtype
+ *   B, C   : [batch, K, N, L] (outputs), dtype
+ *   dtype  : VMB_F32 or VMB_BF16 (outputs rounded to nearest even)
+ * Sizes: N in {1, 2, 4, 8, 16}; 1 <= R <= 64 (a rank of ceil(channels / 32)
+ *   covers inner widths up to 2048).
+ * Errors: VMB_ERR_NULL (u, W, delta, B or C NULL), VMB_ERR_SHAPE (sizes),
+ * VMB_ERR_UNSUPPORTED (N, R, or W_dt NULL with R != 1), VMB_ERR_DTYPE,
+ * VMB_ERR_ALIGN (a base pointer of u, delta, B, C not 16-byte aligned, of
+ * W or W_dt not 4-byte aligned), VMB_ERR_ALIAS (an output overlaps an input
+ * or another output).
+ */
+vmb_status vmb_ss2d_projections(const void* u, const float* W, const float* W_dt, void* delta,
+                                void* B, void* C, int64_t batch, int64_t K, int64_t channels,
+                                int64_t L, int64_t N, int64_t R, vmb_dtype dtype,
+                                vmb_stream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* vmb_status_string(vmb_status s);
 

@@ -118,6 +118,17 @@ vmb_status vmb_mean_scan_fwd_ex(const void* u, const void* delta, const float* A
     return launch_mean_scan(a);
 }
 
+vmb_status vmb_ss2d_projections(const void* u, const float* W, const float* W_dt, void* delta,
+                                void* B, void* C, int64_t batch, int64_t K, int64_t channels,
+                                int64_t L, int64_t N, int64_t R, vmb_dtype dtype,
+                                vmb_stream_t stream) {
+    const vmb_status st = validate_projections(u, W, W_dt, delta, B, C, batch, K, channels, L, N,
+                                               R, dtype);
+    if (st != VMB_OK) return st;
+    return launch_projections(u, W, W_dt, delta, B, C, batch, K, channels, L, N, R, dtype,
+                              static_cast<hipStream_t>(stream));
+}
+
 size_t vmb_scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                                 int64_t L, int64_t N, vmb_layout layout) {
     return scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout);

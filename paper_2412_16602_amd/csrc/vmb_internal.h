@@ -43,6 +43,10 @@ vmb_status validate_channel_mean(const float* x, const float* xm, int64_t batch,
                                  int64_t L);
 size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                             int64_t L, int64_t N, vmb_layout layout);
+vmb_status validate_projections(const void* u, const float* W, const float* W_dt,
+                                const void* delta, const void* B, const void* C, int64_t batch,
+                                int64_t K, int64_t channels, int64_t L, int64_t N, int64_t R,
+                                vmb_dtype dt);
 
 // Chunk length (positions) of the mean variant's reduce / carry / finish passes.
 constexpr int kMeanChunk = 64;
@@ -130,6 +134,10 @@ vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t ch
                               int64_t H, int64_t W, vmb_dtype in_dt, vmb_dtype out_dt,
                               hipStream_t s);
 vmb_status launch_full_scan(const ScanArgs& a);
+// Selection projections of eq. 6 (projections.hip).
+vmb_status launch_projections(const void* u, const float* W, const float* W_dt, void* delta,
+                              void* B, void* C, int64_t batch, int64_t K, int64_t channels,
+                              int64_t L, int64_t N, int64_t R, vmb_dtype dt, hipStream_t s);
 // One-state scan on materialised inputs and the channel mean (scan_discrete.hip).
 vmb_status launch_discrete_scan(const float* abar, const float* bu, const float* C,
                                 const float* skip, float* y, int64_t batch, int64_t channels,

@@ -91,6 +91,35 @@ vmb_status validate_channel_mean(const float* x, const float* xm, int64_t batch,
     return VMB_OK;
 }
 
+vmb_status validate_projections(const void* u, const float* W, const float* W_dt,
+                                const void* delta, const void* B, const void* C, int64_t batch,
+                                int64_t K, int64_t channels, int64_t L, int64_t N, int64_t R,
+                                vmb_dtype dt) {
+    if (!u || !W || !delta || !B || !C) return VMB_ERR_NULL;
+    if (!valid_dtype(dt)) return VMB_ERR_DTYPE;
+    if (batch < 1 || K < 1 || channels < 1 || L < 1 || N < 1 || R < 1 || L > kMaxRow)
+        return VMB_ERR_SHAPE;
+    const int64_t seq = prod({batch, K, channels, L});
+    const int64_t bc = prod({batch, K, N, L});
+    const int64_t wn = prod({K, R + 2 * N, channels});
+    const int64_t wd = prod({K, channels, R});
+    if (seq < 0 || bc < 0 || wn < 0 || wd < 0 || prod({channels, L}) > kMaxRow) return VMB_ERR_SHAPE;
+    if (!supported_n(N) || R > 64 || (!W_dt && R != 1)) return VMB_ERR_UNSUPPORTED;
+    if (!aligned(u, 16) || !aligned(delta, 16) || !aligned(B, 16) || !aligned(C, 16) ||
+        !aligned(W, 4) || (W_dt && !aligned(W_dt, 4)))
+        return VMB_ERR_ALIGN;
+    const size_t e = dsize(dt);
+    const Range outs[] = {range_of(delta, seq, e), range_of(B, bc, e), range_of(C, bc, e)};
+    const Range ins[] = {range_of(u, seq, e), range_of(W, wn, 4),
+                         W_dt ? range_of(W_dt, wd, 4) : Range{0, 0}};
+    for (const Range& o : outs)
+        for (const Range& i : ins)
+            if (overlap(o, i)) return VMB_ERR_ALIAS;
+    if (overlap(outs[0], outs[1]) || overlap(outs[0], outs[2]) || overlap(outs[1], outs[2]))
+        return VMB_ERR_ALIAS;
+    return VMB_OK;
+}
+
 size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                             int64_t L, int64_t N, vmb_layout layout) {
     if (batch < 1 || K < 1 || channels < 1 || L < 1 || N < 1) return SIZE_MAX;

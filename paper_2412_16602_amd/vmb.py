@@ -65,6 +65,8 @@ def load_library():
         fn = getattr(lib, name)
         fn.argtypes = scan[:-1] + [ctypes.c_uint, P]
         fn.restype = I
+    lib.vmb_ss2d_projections.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I, P]
+    lib.vmb_ss2d_projections.restype = I
     lib.vmb_discrete_scan.argtypes = [P, P, P, P, P, I64, I64, I64, P]
     lib.vmb_discrete_scan.restype = I
     lib.vmb_channel_mean.argtypes = [P, P, I64, I64, I64, P]
@@ -246,6 +248,36 @@ def vmb_mean_scan_fwd_ex(u, delta, A, B, C, D, dt_bias, delta_softplus, y, optio
     y is [batch, K, 1, L] with VMB_MEAN_NO_BROADCAST). Returns y."""
     return _scan("vmb_mean_scan_fwd_ex", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
                  y, layout, workspace, stream, options=options)
+
+
+def vmb_ss2d_projections(u: torch.Tensor, W: torch.Tensor, W_dt: Optional[torch.Tensor],
+                         delta: torch.Tensor, B: torch.Tensor, C: torch.Tensor,
+                         stream=None):
+    """Selection projections of eq. 6: u [batch, K, channels, L] ->
+    delta [batch, K, channels, L], B, C [batch, K, N, L]; W float32
+    [K, R + 2N, channels], W_dt float32 [K, channels, R] or None (R = 1,
+    broadcast). Returns (delta, B, C)."""
+    lib = load_library()
+    batch, K, channels, L = u.shape
+    N = B.shape[2]
+    R = W.shape[1] - 2 * N
+    if tuple(W.shape) != (K, R + 2 * N, channels):
+        raise ValueError(f"W shape {tuple(W.shape)} != {(K, R + 2 * N, channels)}")
+    if W_dt is not None and tuple(W_dt.shape) != (K, channels, R):
+        raise ValueError(f"W_dt shape {tuple(W_dt.shape)} != {(K, channels, R)}")
+    if tuple(delta.shape) != tuple(u.shape):
+        raise ValueError("delta must have the shape of u")
+    for t, nm in ((B, "B"), (C, "C")):
+        if tuple(t.shape) != (batch, K, N, L):
+            raise ValueError(f"{nm} shape {tuple(t.shape)} != {(batch, K, N, L)}")
+    for t, nm in ((delta, "delta"), (B, "B"), (C, "C")):
+        if t.dtype != u.dtype:
+            raise ValueError(f"{nm} must have the dtype of u")
+    _check(lib.vmb_ss2d_projections(_dev(u, "u"), _f32(W, "W"), _f32(W_dt, "W_dt"),
+                                    _dev(delta, "delta"), _dev(B, "B"), _dev(C, "C"), batch, K,
+                                    channels, L, N, R, _dtype(u, "u"), _stream(stream)),
+           "vmb_ss2d_projections")
+    return delta, B, C
 
 
 def vmb_discrete_scan(abar: torch.Tensor, bu: torch.Tensor, C: torch.Tensor,
