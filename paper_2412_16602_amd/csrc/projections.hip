@@ -18,7 +18,12 @@
 // are flattened over (batch, t): a workgroup owns P = 16 CB consecutive
 // flattened positions of one direction (CB = 1, 2 or 4 column blocks of 16,
 // chosen on the host so that the grid fills the chip), and short sequences
-// still fill whole tiles.
+// still fill whole tiles. A tile of 16 or 32 positions reads only part of
+// each 128-byte line of a channel row; its neighbours read the rest. The
+// dispatcher deals workgroups to the eight XCDs (each with its own L2)
+// round-robin, so the 1-D grid is remapped to give each XCD a contiguous
+// range of tiles: neighbours then share one L2 instead of each XCD fetching
+// the line again.
 //   1. x_dbl: the channels are walked in chunks of 64; each chunk of u and of
 //      W is staged in LDS (row strides padded by one word: the MFMA operand
 //      reads are conflict-free) while the next chunk is already being loaded
@@ -60,7 +65,7 @@ template <typename T, int MB, int CB>
 __global__ __launch_bounds__(256) void k_projections(
     const T* __restrict__ u, const float* __restrict__ W, const float* __restrict__ Wdt,
     T* __restrict__ delta, T* __restrict__ Bo, T* __restrict__ Co, int K, int Dc, int L, int N,
-    int R, int64_t positions) {
+    int R, int64_t positions, int tiles) {
     constexpr int P = 16 * CB;   // positions per workgroup
     constexpr int PP = P + 1;    // LDS row stride of the u chunk and the timescale rows
     constexpr int KS = 4 / CB;   // channel slices
@@ -73,8 +78,13 @@ __global__ __launch_bounds__(256) void k_projections(
     float* su = pool;
     float* sw = pool + kUsz;
 
-    const int k = blockIdx.y;
-    const int64_t p0 = static_cast<int64_t>(blockIdx.x) * P;
+    // XCD-contiguous tile order: workgroup i runs on XCD i % 8; XCD x takes
+    // tiles [x q + min(x, rem), ...) of the K * tiles in (k, tile) order
+    const int nwg = static_cast<int>(gridDim.x), wg = static_cast<int>(blockIdx.x);
+    const int q = nwg / 8, rem = nwg % 8, xcd = wg % 8, idx = wg / 8;
+    const int logical = xcd * q + (xcd < rem ? xcd : rem) + idx;
+    const int k = logical / tiles;
+    const int64_t p0 = static_cast<int64_t>(logical - k * tiles) * P;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int col = lane & 15, kq = lane >> 4;  // MFMA operand coordinates
@@ -249,11 +259,11 @@ int column_blocks(int64_t positions, int64_t K) {
 template <typename T, int MB, int CB>
 void launch_mb(int64_t positions, hipStream_t s, const void* u, const float* W, const float* W_dt,
                void* delta, void* B, void* C, int K, int Dc, int L, int N, int R) {
-    const dim3 grid(static_cast<unsigned>((positions + 16 * CB - 1) / (16 * CB)),
-                    static_cast<unsigned>(K));
-    hipLaunchKernelGGL((k_projections<T, MB, CB>), grid, dim3(256), 0, s,
-                       static_cast<const T*>(u), W, W_dt, static_cast<T*>(delta),
-                       static_cast<T*>(B), static_cast<T*>(C), K, Dc, L, N, R, positions);
+    const int64_t tiles = (positions + 16 * CB - 1) / (16 * CB);
+    hipLaunchKernelGGL((k_projections<T, MB, CB>), dim3(static_cast<unsigned>(tiles * K)),
+                       dim3(256), 0, s, static_cast<const T*>(u), W, W_dt, static_cast<T*>(delta),
+                       static_cast<T*>(B), static_cast<T*>(C), K, Dc, L, N, R, positions,
+                       static_cast<int>(tiles));
 }
 
 template <typename T, int CB>
@@ -286,8 +296,7 @@ vmb_status launch_projections(const void* u, const float* W, const float* W_dt, 
                               void* B, void* C, int64_t batch, int64_t K, int64_t channels,
                               int64_t L, int64_t N, int64_t R, vmb_dtype dt, hipStream_t s) {
     const int64_t positions = batch * L;
-    if (R > kMaxR || R + 2 * N > 16 * kMaxMB || K > 65535 ||
-        (positions + 15) / 16 > int64_t{0x7fffffff})
+    if (R > kMaxR || R + 2 * N > 16 * kMaxMB || (positions + 15) / 16 * K > int64_t{0x7fffffff})
         return VMB_ERR_UNSUPPORTED;
     const int mb = static_cast<int>((R + 2 * N + 15) / 16);
     if (dt == VMB_F32)
