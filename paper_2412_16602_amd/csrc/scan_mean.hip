@@ -83,6 +83,7 @@ struct MeanWs {
     float* agg;
     float* carry;
     float* ytil;  // 2-D layout: reduced output ytilde[bk][t]
+    float* gpart; // channel-group partial sums (split reduce)
 };
 
 // How the reduced output leaves (sequence layout): skip_own adds each
@@ -117,9 +118,11 @@ __device__ __forceinline__ void store_reduced(float yt, Tout* __restrict__ y,
     for (int d = d0 + wv; d < d1; d += step) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
 }
 
-// Reduce stage of one chunk (chunk blockIdx.x of sequence (blockIdx.z,
-// blockIdx.y)): every wave's partial sums over its channels, for the lanes'
-// positions, left in part[wv][0..N+2) (exp sums per state, s, r).
+// Reduce stage of one chunk (chunk blockIdx.x / groups of sequence
+// (blockIdx.z, blockIdx.y), channel group blockIdx.x % groups): every wave's
+// partial sums over its channels (a 1 / (16 groups) slice of the sequence's
+// channels), for the lanes' positions, left in part[wv][0..N+2) (exp sums
+// per state, s, r).
 // A wave's partial sums fill N + 2 rows (exp sums per state, s, r), one more
 // (the input sum) when T averages the raw terms, N more (the sums of the
 // zero-order-hold terms phi(Delta A_n) Delta u, rows N + 2 ..) with kZoh.
@@ -132,7 +135,8 @@ template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh = false>
 __device__ __forceinline__ void reduce_partials(
     float (*part)[(part_rows<N, kRaw, kZoh>())][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
     const float* __restrict__ A, const float* __restrict__ D, const float* __restrict__ dt_bias,
-    const Tin* __restrict__ xt, int K, int Dc, int L, int H, int W, int C, int softplus) {
+    const Tin* __restrict__ xt, int K, int Dc, int L, int H, int W, int C, int softplus,
+    int groups = 1) {
     // Each wave's slice part[wv] first holds its channel parameters (two
     // buffers of kAhead rows: A[c, 0..N) log2(e), dt_bias[c], D[c], and with
     // kZoh 1 / A[c, 0..N)), read back as wave-uniform broadcasts, and
@@ -140,7 +144,8 @@ __device__ __forceinline__ void reduce_partials(
     constexpr int kPS = (N + 2 + (kZoh ? N : 0) + 3) & ~3;  // parameter row stride (16-byte rows)
     static_assert(2 * kAhead * kPS <= (N + 2) * kC, "parameter buffers fit a wave's slice");
     static_assert(kAhead <= 32, "parameter row layout");
-    const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
+    const int chunk = blockIdx.x / groups, grp = blockIdx.x % groups;
+    const int k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
     const int t = chunk * C + lane;
@@ -163,7 +168,8 @@ __device__ __forceinline__ void reduce_partials(
 #pragma unroll
     for (int n = 0; n < (kZoh ? N : 1); ++n) zacc[n] = 0.0f;
     float s = 0.0f, r = 0.0f, q = 0.0f;
-    const int d0 = (wv * Dc) / kRedWaves, d1 = ((wv + 1) * Dc) / kRedWaves;
+    const int slice = grp * kRedWaves + wv, nslices = kRedWaves * groups;
+    const int d0 = (slice * Dc) / nslices, d1 = ((slice + 1) * Dc) / nslices;
     const int nw = d1 - d0;  // channels of this wave
     float* prm = &part[wv][0][0];
     const size_t cw = static_cast<size_t>(k) * Dc + d0;  // parameter row of the wave's first channel
@@ -339,17 +345,14 @@ __device__ __forceinline__ void reduced_pair(const float (*part)[(part_rows<N, k
     }
 }
 
-template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh>
-__global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
-    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
-    const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
-    const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
-    int softplus) {
-    __shared__ __align__(16) float part[kRedWaves][(part_rows<N, kRaw, kZoh>())][kC];
-    reduce_partials<N, Tin, kTwoD, kRaw, kZoh>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
-                                               softplus);
-    __syncthreads();
-    const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
+// Chunk-local scan of one chunk from the channel sums in part (slots added
+// in slot order): r_mean, then wave w scans states w, w + 16, ... and stores
+// the per-position pairs and the chunk aggregate.
+template <int N, typename Tin, bool kRaw, bool kZoh>
+__device__ __forceinline__ void scan_chunk(const float (*part)[(part_rows<N, kRaw, kZoh>())][kC],
+                                           const Tin* __restrict__ Bm, MeanWs ws, int K, int Dc,
+                                           int L, int C, int nchunks, int chunk) {
+    const int k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
     const int t = chunk * C + lane;
@@ -357,8 +360,6 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const int tc = valid ? t : L - 1;
     const size_t bk = static_cast<size_t>(b) * K + k;
 
-    // channel groups added in a fixed order; wave w then scans states
-    // w, w + 16, ... of this chunk
     const float inv = 1.0f / static_cast<float>(Dc);
     if (wv == 0) {
         float rm = 0.0f;
@@ -382,6 +383,55 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
             *reinterpret_cast<float2*>(agg_bk + (static_cast<size_t>(n) * nchunks + chunk) * 2) =
                 make_float2(a, bb);
     }
+}
+
+// With groups == 1 the reduce scans its chunk itself; otherwise each of the
+// groups workgroups of a chunk stores its channel group's sums (its waves
+// added in wave order) for k_mean_combine.
+template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh>
+__global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
+    const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
+    const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
+    const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
+    int softplus, int groups) {
+    constexpr int kRows = part_rows<N, kRaw, kZoh>();
+    __shared__ __align__(16) float part[kRedWaves][kRows][kC];
+    reduce_partials<N, Tin, kTwoD, kRaw, kZoh>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
+                                               softplus, groups);
+    __syncthreads();
+    if (groups == 1) {
+        scan_chunk<N, Tin, kRaw, kZoh>(part, Bm, ws, K, Dc, L, C, nchunks, blockIdx.x);
+        return;
+    }
+    const int chunk = blockIdx.x / groups, grp = blockIdx.x % groups;
+    const int lane = threadIdx.x % kC;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kC);
+    const size_t bkc = (static_cast<size_t>(blockIdx.z) * K + blockIdx.y) * nchunks + chunk;
+    float* gp = ws.gpart + ((bkc * groups + grp) * kRows) * kC;
+    for (int r = wv; r < kRows; r += kRedWaves) {
+        float sum = 0.0f;
+        for (int w = 0; w < kRedWaves; ++w) sum += part[w][r][lane];
+        gp[r * kC + lane] = sum;
+    }
+}
+
+// Combine of the split reduce: chunk blockIdx.x of sequence (blockIdx.z,
+// blockIdx.y) takes its groups' sums as the first slots of part (the other
+// slots zero), then scans the chunk as the unsplit reduce does.
+template <int N, typename Tin, bool kRaw, bool kZoh>
+__global__ __launch_bounds__(kC* kRedWaves) void k_mean_combine(const Tin* __restrict__ Bm,
+                                                                MeanWs ws, int K, int Dc, int L,
+                                                                int C, int nchunks, int groups) {
+    constexpr int kRows = part_rows<N, kRaw, kZoh>();
+    __shared__ __align__(16) float part[kRedWaves][kRows][kC];
+    const size_t bkc =
+        (static_cast<size_t>(blockIdx.z) * K + blockIdx.y) * nchunks + blockIdx.x;
+    const float* gp = ws.gpart + bkc * groups * kRows * kC;
+    float* pf = &part[0][0][0];
+    for (int i = threadIdx.x; i < kRedWaves * kRows * kC; i += kC * kRedWaves)
+        pf[i] = i < groups * kRows * kC ? gp[i] : 0.0f;
+    __syncthreads();
+    scan_chunk<N, Tin, kRaw, kZoh>(part, Bm, ws, K, Dc, L, C, nchunks, blockIdx.x);
 }
 
 // One wave per (batch, k, n): exclusive scan of the chunk aggregates.
@@ -856,6 +906,7 @@ vmb_status run(const ScanArgs& a) {
     ws.agg = reinterpret_cast<float*>(p + lay.agg);
     ws.carry = reinterpret_cast<float*>(p + lay.carry);
     ws.ytil = kTwoD ? reinterpret_cast<float*>(p + lay.ytil) : nullptr;
+    ws.gpart = reinterpret_cast<float*>(p + lay.gpart);
 
     const int K = int(a.K), Dc = int(a.channels), L = int(a.L), H = int(a.H), W = int(a.W);
     const int C = mean_chunk(a.batch, a.K, a.L);
@@ -867,7 +918,9 @@ vmb_status run(const ScanArgs& a) {
     const long long wgs = static_cast<long long>(nchunks) * a.K * a.batch;
     // (the zero-order-hold sums need more LDS than the one-launch kernel has
     // room for next to its other buffers: those calls take the three passes)
-    const bool fused = !kZoh && C == kC && nchunks <= kWave && (nchunks == 1 || wgs <= kFusedMaxGrid);
+    const int rgroups = mean_groups(a.batch, a.K, a.channels, a.L);  // reduce channel groups
+    const bool fused = !kZoh && rgroups == 1 && C == kC && nchunks <= kWave &&
+                       (nchunks == 1 || wgs <= kFusedMaxGrid);
     const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
     // 2-D layout: column-major copies of the planes first, so that every
     // direction's reduce reads stay coalesced
@@ -892,13 +945,21 @@ vmb_status run(const ScanArgs& a) {
         if (sf != VMB_OK || !kTwoD) return sf;
         return launch_merge_broadcast<Tin, Tout>(ws.ytil, a);
     }
-    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD, kRaw, kZoh>), grid, dim3(kC * kRedWaves), 0,
-                       a.stream,
+    hipLaunchKernelGGL((k_mean_reduce<N, Tin, kTwoD, kRaw, kZoh>),
+                       dim3(nchunks * rgroups, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch)),
+                       dim3(kC * kRedWaves), 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), a.D, a.dt_bias, xt, ws, K, Dc, L, H, W, C,
-                       nchunks, a.softplus);
+                       nchunks, a.softplus, rgroups);
     vmb_status st = check_launch();
     if (st != VMB_OK) return st;
+    if (rgroups > 1) {
+        hipLaunchKernelGGL((k_mean_combine<N, Tin, kRaw, kZoh>), grid, dim3(kC * kRedWaves), 0,
+                           a.stream, static_cast<const Tin*>(a.B), ws, K, Dc, L, C, nchunks,
+                           rgroups);
+        st = check_launch();
+        if (st != VMB_OK) return st;
+    }
     const int inline_carry = nchunks <= kWave ? 1 : 0;
     if (!inline_carry) {
         hipLaunchKernelGGL(k_mean_carry, dim3(static_cast<unsigned>(bkn * N)), dim3(kWave), 0,

@@ -57,6 +57,24 @@ constexpr int kMeanChunk = 64;
 // lines) at no cost in parallelism: the per-SIMD channel work is the same.
 inline int mean_chunk(int64_t /*batch*/, int64_t /*K*/, int64_t /*L*/) { return kMeanChunk; }
 
+// Channel groups of the mean's reduce pass. One 16-wave workgroup per chunk
+// of a (batch, direction) sequence leaves most compute units idle when there
+// are few chunks (7x7 maps: one per sequence); the channels of a chunk are
+// then split over G workgroups, whose partial sums a combine pass adds in
+// group order. G fills about two workgroups per compute unit and leaves each
+// wave at least four channels.
+constexpr int64_t kMeanSplitBelow = 160;  // chunk-sequence workgroups below which to split
+// (at 196, the 56x56 map, the one-launch path is faster: 16.8 us against 28.2 split in three)
+constexpr int kMeanMaxGroups = 16;
+inline int mean_groups(int64_t batch, int64_t K, int64_t channels, int64_t L) {
+    const int64_t wgs = (L + kMeanChunk - 1) / kMeanChunk * K * batch;
+    if (wgs >= kMeanSplitBelow) return 1;
+    int64_t g = (512 + wgs - 1) / wgs;
+    if (g > kMeanMaxGroups) g = kMeanMaxGroups;
+    if (g > channels / 64) g = channels / 64;
+    return g > 1 ? static_cast<int>(g) : 1;
+}
+
 // Byte offsets of the mean variant's workspace regions (each 256-byte
 // aligned), for bk = batch * K direction sequences of L positions:
 //   scan  [bk][N][L][2] float : chunk-local inclusive scan (P, H)
@@ -66,10 +84,13 @@ inline int mean_chunk(int64_t /*batch*/, int64_t /*K*/, int64_t /*L*/) { return 
 //   ytil  [bk][L]             : 2-D layout only, the reduced output
 //   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL only,
 //                               column-major copies of the input planes
+//   flags [bk][nch]     u64   : one-launch path's chunk flags
+//   gpart [bk][nch][G][2N+3][64] : with G = mean_groups(..) > 1 only, each
+//                               channel group's partial sums of a chunk
 constexpr int64_t kMeanTransposeMaxL = 6144;  // then H * (W + 1) <= 2 L fits LDS
 static_assert(kMeanTransposeMaxL == 6144, "full_ws_has_xt uses the same bound");
 struct MeanWsLayout {
-    size_t scan, rmean, agg, carry, ytil, xt, flags, total;
+    size_t scan, rmean, agg, carry, ytil, xt, flags, gpart, total;
 };
 inline bool mean_transposes(int64_t L, bool two_d) { return two_d && L <= kMeanTransposeMaxL; }
 inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, int64_t L,
@@ -87,7 +108,11 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, i
     o.xt = o.ytil + (two_d ? up(bk * L * 4) : 0);
     const size_t planes = static_cast<size_t>(batch) * static_cast<size_t>(channels);
     o.flags = o.xt + (mean_transposes(L, two_d) ? up(planes * L * 4) : 0);
-    o.total = o.flags + up(bk * nch * 8);  // one 64-bit flag per chunk
+    o.gpart = o.flags + up(bk * nch * 8);  // one 64-bit flag per chunk
+    const size_t groups = static_cast<size_t>(mean_groups(batch, K, channels, L));
+    o.total = o.gpart +
+              (groups > 1 ? up(bk * nch * groups * static_cast<size_t>(2 * N + 3) * kMeanChunk * 4)
+                          : 0);
     return o;
 }
 
