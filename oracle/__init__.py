@@ -209,6 +209,31 @@ def projections(u, W, W_dt=None, N: int = 16):
     return delta, np.ascontiguousarray(B), np.ascontiguousarray(C)
 
 
+def out_norm_gate(y, z=None, gamma=None, beta=None, eps: float = 1e-5):
+    """The step after the cross-merge in VMamba's SS2D block (not in the
+    paper's text): a layer normalisation over the channels of each pixel,
+    then, with z given, the gate z * sigmoid(z) (SiLU), fp64:
+      mu[b,p]    = mean_d y[b,d,p]
+      var[b,p]   = mean_d (y[b,d,p] - mu[b,p])^2          (biased)
+      out[b,d,p] = (y[b,d,p] - mu[b,p]) / sqrt(var[b,p] + eps) * gamma[d] + beta[d]
+      out[b,d,p] *= z[b,d,p] / (1 + exp(-z[b,d,p]))        (z given)
+    y, z [batch, Dc, P] (P = H*W, the 2-D layout); gamma, beta [Dc] or None
+    (1 and 0). Returns out [batch, Dc, P] as float64.
+    """
+    y = np.asarray(y, dtype=np.float64)
+    mu = y.mean(axis=1, keepdims=True)
+    var = ((y - mu) ** 2).mean(axis=1, keepdims=True)
+    out = (y - mu) / np.sqrt(var + eps)
+    if gamma is not None:
+        out = out * np.asarray(gamma, dtype=np.float64)[None, :, None]
+    if beta is not None:
+        out = out + np.asarray(beta, dtype=np.float64)[None, :, None]
+    if z is not None:
+        z = np.asarray(z, dtype=np.float64)
+        out = out * (z / (1.0 + np.exp(-z)))
+    return out
+
+
 def discrete_scan(abar, bu, C, skip=None, nthreads: int = 0) -> np.ndarray:
     """One-state scan on materialised inputs in fp64.
 

@@ -798,3 +798,71 @@ def test_projections_broadcast_timescale():
         ref = pw.W[k, 0].astype(np.float64) @ u[0, k].astype(np.float64)
         for d in range(5):
             np.testing.assert_allclose(delta[0, k, d], ref, rtol=1e-14, atol=1e-15)
+
+
+# ---- the post-merge channel normalisation and gate (VMamba's SS2D step after
+# the cross-merge; not in the paper's text, so pinned by definition and a
+# library routine, not by paper values)
+
+def test_out_norm_matches_torch_layer_norm():
+    """Channel LayerNorm per pixel = torch's layer_norm over the last axis of
+    the channel-last transpose (an independent library routine), fp64."""
+    import torch
+
+    rng = np.random.default_rng(70)
+    b, Dc, P = 2, 9, 13
+    y = rng.standard_normal((b, Dc, P)) * 3.0 + 1.5
+    g = rng.standard_normal(Dc)
+    be = rng.standard_normal(Dc)
+    got = oracle.out_norm_gate(y, None, g, be, eps=1e-3)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(y).permute(0, 2, 1), (Dc,),
+                                         torch.from_numpy(g), torch.from_numpy(be), 1e-3)
+    np.testing.assert_allclose(got, ref.permute(0, 2, 1).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_out_norm_hand_example():
+    """One pixel, channels (1, 2, 3), eps 0: mean 2, biased variance 2/3, so the
+    output is (-sqrt(3/2), 0, sqrt(3/2)); gamma (2, 2, 2) and beta (1, 1, 1)
+    map it to 1 -+ sqrt(6)."""
+    y = np.array([1.0, 2.0, 3.0]).reshape(1, 3, 1)
+    got = oracle.out_norm_gate(y, eps=0.0)[0, :, 0]
+    np.testing.assert_allclose(got, [-np.sqrt(1.5), 0.0, np.sqrt(1.5)], rtol=1e-15, atol=1e-15)
+    got = oracle.out_norm_gate(y, None, np.full(3, 2.0), np.ones(3), eps=0.0)[0, :, 0]
+    np.testing.assert_allclose(got, [1 - np.sqrt(6), 1.0, 1 + np.sqrt(6)], rtol=1e-15)
+
+
+def test_out_norm_invariants():
+    """gamma 1, beta 0, eps 0: every pixel's output has mean 0 and variance 1,
+    and is unchanged by a positive scale and a per-pixel shift of y (the
+    normalisation runs over channels, not pixels: a per-channel shift would
+    change it)."""
+    rng = np.random.default_rng(71)
+    y = rng.standard_normal((3, 11, 7))
+    out = oracle.out_norm_gate(y, eps=0.0)
+    np.testing.assert_allclose(out.mean(axis=1), 0.0, atol=1e-14)
+    np.testing.assert_allclose((out ** 2).mean(axis=1), 1.0, rtol=1e-13)
+    shift = rng.standard_normal((3, 1, 7))
+    np.testing.assert_allclose(oracle.out_norm_gate(2.5 * y + shift, eps=0.0), out, atol=1e-12)
+    per_channel = rng.standard_normal((1, 11, 1))
+    assert not np.allclose(oracle.out_norm_gate(y + per_channel, eps=0.0), out, atol=1e-3)
+
+
+def test_out_gate_silu():
+    """The gate is z * sigmoid(z). Textbook values: silu(1) = e / (1 + e),
+    silu(-1) = -(1 - e / (1 + e)), silu(2) = 2 e^2 / (1 + e^2), silu(0) = 0; the mirrored form
+    z * sigmoid(-z) gives 1 / (1 + e) at z = 1 and fails. The odd part
+    silu(z) - silu(-z) = z holds for any z."""
+    e = np.e
+    y = np.array([1.0, 2.0, 3.0]).reshape(1, 3, 1)  # normalises to (-a, 0, a), a = sqrt(3/2)
+    a = np.sqrt(1.5)
+    for zv, silu in ((1.0, e / (1 + e)), (-1.0, -(1 - e / (1 + e))), (2.0, 2 * e * e / (1 + e * e))):
+        z = np.full((1, 3, 1), zv)
+        got = oracle.out_norm_gate(y, z, eps=0.0)[0, :, 0]
+        np.testing.assert_allclose(got, [-a * silu, 0.0, a * silu], rtol=1e-14, atol=1e-15)
+    rng = np.random.default_rng(72)
+    y = rng.standard_normal((1, 5, 6))
+    z = rng.standard_normal((1, 5, 6)) * 4.0
+    n = oracle.out_norm_gate(y, eps=1e-5)
+    diff = oracle.out_norm_gate(y, z, eps=1e-5) - oracle.out_norm_gate(y, -z, eps=1e-5)
+    np.testing.assert_allclose(diff, n * z, rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(oracle.out_norm_gate(y, np.zeros_like(y)), 0.0)
