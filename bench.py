@@ -570,6 +570,64 @@ def projections_bench(steps: int, warmup: int):
             "rows": rows}
 
 
+def out_norm_bench(steps: int, warmup: int):
+    """The channel normalisation and SiLU gate after the cross-merge
+    (vmb_ss2d_out_norm) at every N = 16 workload's merged output
+    [batch, channels, H*W]: us per call with HIP events on the launch stream,
+    inputs rotated past the MALL; algorithmic bytes are y and z read and out
+    written once."""
+    import torch
+
+    from paper_2412_16602_amd import vmb
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+    rows = []
+    for shp in (workloads.STAGE1, workloads.STAGE2, workloads.STAGE3, workloads.STAGE4,
+                workloads.BATCHED_BF16, workloads.HIRES):
+        b, Dc, P = shp.batch, shp.channels, shp.H * shp.W
+        dt = torch.bfloat16 if shp.dtype == "bf16" else torch.float32
+        esz = 2 if shp.dtype == "bf16" else 4
+        nbytes = 3 * b * Dc * P * esz
+        n_sets = max(1, min(8, -(-ROTATE_BYTES // nbytes)))
+        sets = [(torch.randn(b, Dc, P, device=dev, generator=g).to(dt),
+                 torch.randn(b, Dc, P, device=dev, generator=g).to(dt)) for _ in range(n_sets)]
+        gamma = 1 + 0.1 * torch.randn(Dc, device=dev, generator=g)
+        beta = 0.1 * torch.randn(Dc, device=dev, generator=g)
+        out = torch.empty(b, Dc, P, device=dev, dtype=dt)
+
+        def call(i):
+            y, z = sets[i % n_sets]
+            vmb.vmb_ss2d_out_norm(y, z, gamma, beta, 1e-5, out, stream=stream)
+        for i in range(warmup):
+            call(i)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        call(0)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        n = max(3, min(steps, int(0.2e6 / max(1.0, e0.elapsed_time(e1) * 1e3))))
+        e0.record(stream)
+        for i in range(n):
+            call(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / n
+        rows.append({"workload": shp.name, "dtype": shp.dtype, "us": round(us, 2), "calls": n,
+                     "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                     "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)})
+        del sets, out
+        torch.cuda.empty_cache()
+    return {"metric": "channel LayerNorm + SiLU gate after the merge, every N=16 workload (us/call)",
+            "unit": "us/call", "data": "synthetic",
+            "timing": "HIP events on the launch stream around consecutive calls",
+            "rows": rows}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -599,6 +657,9 @@ def main():
     ap.add_argument("--projections", action="store_true",
                     help="after the main line, print a line timing the selection projections "
                          "of eq. 6 at every N=16 workload")
+    ap.add_argument("--outnorm", action="store_true",
+                    help="after the main line, print a line timing the channel LayerNorm and "
+                         "SiLU gate after the merge at every N=16 workload")
     ap.add_argument("--table1", action="store_true",
                     help="after the main line, print a second JSON line: the one-state scan "
                          "on materialised inputs at the paper's Table 1 shapes")
@@ -666,6 +727,8 @@ def main():
         print(json.dumps(workloads_bench(args.steps, 3)), flush=True)
     if args.projections:
         print(json.dumps(projections_bench(args.steps, 3)), flush=True)
+    if args.outnorm:
+        print(json.dumps(out_norm_bench(args.steps, 3)), flush=True)
     if args.table1:
         print(json.dumps(table1_bench(max(5, args.steps // 10), 3)), flush=True)
 

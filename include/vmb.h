@@ -316,6 +316,30 @@ vmb_status vmb_ss2d_projections(const void* u, const float* W, const float* W_dt
                                 int64_t L, int64_t N, int64_t R, vmb_dtype dtype,
                                 vmb_stream_t stream);
 
+/*
+ * The step after the cross-merge in VMamba's SS2D block, which the paper's
+ * models are built from (the paper's text ends the SS2D computation at the
+ * merge of Appendix A): a layer normalisation over the channels of each
+ * pixel, then the SiLU gate by a second branch z. Per pixel p of image b:
+ *   mu[b,p]    = mean_d y[b,d,p],  var[b,p] = mean_d (y[b,d,p] - mu[b,p])^2
+ *   out[b,d,p] = (y[b,d,p] - mu[b,p]) / sqrt(var[b,p] + eps) * gamma[d] + beta[d]
+ *   out[b,d,p] *= z[b,d,p] / (1 + exp(-z[b,d,p]))       (z not NULL)
+ * Statistics in binary32 (a mean pass, then the centred sum of squares).
+ *
+ *   y, out : [batch, channels, P] (the 2-D layout, P = H * W), dtype
+ *   z      : [batch, channels, P], dtype, or NULL (no gate)
+ *   gamma, beta : float32 [channels], or NULL (1 and 0)
+ *   eps    : >= 0, finite
+ *   dtype  : VMB_F32 or VMB_BF16 (out rounded to nearest even)
+ * Errors: VMB_ERR_NULL (y or out NULL), VMB_ERR_SHAPE (sizes, eps),
+ * VMB_ERR_DTYPE, VMB_ERR_ALIGN (y, z, out not aligned to their element,
+ * gamma, beta not 4-byte aligned), VMB_ERR_ALIAS (out overlaps y, z, gamma
+ * or beta).
+ */
+vmb_status vmb_ss2d_out_norm(const void* y, const void* z, const float* gamma, const float* beta,
+                             float eps, void* out, int64_t batch, int64_t channels, int64_t P,
+                             vmb_dtype dtype, vmb_stream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* vmb_status_string(vmb_status s);
 

@@ -129,6 +129,16 @@ vmb_status vmb_ss2d_projections(const void* u, const float* W, const float* W_dt
                               static_cast<hipStream_t>(stream));
 }
 
+vmb_status vmb_ss2d_out_norm(const void* y, const void* z, const float* gamma, const float* beta,
+                             float eps, void* out, int64_t batch, int64_t channels, int64_t P,
+                             vmb_dtype dtype, vmb_stream_t stream) {
+    const vmb_status st =
+        validate_out_norm(y, z, gamma, beta, eps, out, batch, channels, P, dtype);
+    if (st != VMB_OK) return st;
+    return launch_out_norm(y, z, gamma, beta, eps, out, batch, channels, P, dtype,
+                           static_cast<hipStream_t>(stream));
+}
+
 size_t vmb_scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                                 int64_t L, int64_t N, vmb_layout layout) {
     return scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout);

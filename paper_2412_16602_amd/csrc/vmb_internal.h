@@ -43,6 +43,9 @@ vmb_status validate_channel_mean(const float* x, const float* xm, int64_t batch,
                                  int64_t L);
 size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                             int64_t L, int64_t N, vmb_layout layout);
+vmb_status validate_out_norm(const void* y, const void* z, const float* gamma, const float* beta,
+                             float eps, const void* out, int64_t batch, int64_t channels,
+                             int64_t P, vmb_dtype dt);
 vmb_status validate_projections(const void* u, const float* W, const float* W_dt,
                                 const void* delta, const void* B, const void* C, int64_t batch,
                                 int64_t K, int64_t channels, int64_t L, int64_t N, int64_t R,
@@ -160,6 +163,9 @@ vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t ch
                               hipStream_t s);
 vmb_status launch_full_scan(const ScanArgs& a);
 // Selection projections of eq. 6 (projections.hip).
+vmb_status launch_out_norm(const void* y, const void* z, const float* gamma, const float* beta,
+                           float eps, void* out, int64_t batch, int64_t channels, int64_t P,
+                           vmb_dtype dt, hipStream_t s);
 vmb_status launch_projections(const void* u, const float* W, const float* W_dt, void* delta,
                               void* B, void* C, int64_t batch, int64_t K, int64_t channels,
                               int64_t L, int64_t N, int64_t R, vmb_dtype dt, hipStream_t s);

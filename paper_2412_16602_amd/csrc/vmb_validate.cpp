@@ -120,6 +120,27 @@ vmb_status validate_projections(const void* u, const float* W, const float* W_dt
     return VMB_OK;
 }
 
+vmb_status validate_out_norm(const void* y, const void* z, const float* gamma, const float* beta,
+                             float eps, const void* out, int64_t batch, int64_t channels,
+                             int64_t P, vmb_dtype dt) {
+    if (!y || !out) return VMB_ERR_NULL;
+    if (!valid_dtype(dt)) return VMB_ERR_DTYPE;
+    if (batch < 1 || channels < 1 || P < 1 || !(eps >= 0.0f) || eps > 3.0e38f)
+        return VMB_ERR_SHAPE;
+    const int64_t n = prod({batch, channels, P});
+    if (n < 0 || prod({channels, P}) > kMaxRow) return VMB_ERR_SHAPE;
+    const size_t e = dsize(dt);
+    if (!aligned(y, e) || !aligned(out, e) || (z && !aligned(z, e)) ||
+        (gamma && !aligned(gamma, 4)) || (beta && !aligned(beta, 4)))
+        return VMB_ERR_ALIGN;
+    const Range o = range_of(out, n, e);
+    if (overlap(o, range_of(y, n, e)) || (z && overlap(o, range_of(z, n, e))) ||
+        (gamma && overlap(o, range_of(gamma, channels, 4))) ||
+        (beta && overlap(o, range_of(beta, channels, 4))))
+        return VMB_ERR_ALIAS;
+    return VMB_OK;
+}
+
 size_t scan_workspace_bytes(int mean_variant, int64_t batch, int64_t K, int64_t channels,
                             int64_t L, int64_t N, vmb_layout layout) {
     if (batch < 1 || K < 1 || channels < 1 || L < 1 || N < 1) return SIZE_MAX;

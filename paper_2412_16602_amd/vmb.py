@@ -67,6 +67,8 @@ def load_library():
         fn.restype = I
     lib.vmb_ss2d_projections.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I, P]
     lib.vmb_ss2d_projections.restype = I
+    lib.vmb_ss2d_out_norm.argtypes = [P, P, P, P, ctypes.c_float, P, I64, I64, I64, I, P]
+    lib.vmb_ss2d_out_norm.restype = I
     lib.vmb_discrete_scan.argtypes = [P, P, P, P, P, I64, I64, I64, P]
     lib.vmb_discrete_scan.restype = I
     lib.vmb_channel_mean.argtypes = [P, P, I64, I64, I64, P]
@@ -278,6 +280,29 @@ def vmb_ss2d_projections(u: torch.Tensor, W: torch.Tensor, W_dt: Optional[torch.
                                     channels, L, N, R, _dtype(u, "u"), _stream(stream)),
            "vmb_ss2d_projections")
     return delta, B, C
+
+
+def vmb_ss2d_out_norm(y: torch.Tensor, z: Optional[torch.Tensor], gamma: Optional[torch.Tensor],
+                      beta: Optional[torch.Tensor], eps: float, out: torch.Tensor, stream=None):
+    """Channel layer normalisation per pixel, then the SiLU gate by z (None:
+    no gate): y, z, out [batch, channels, H, W] (or [batch, channels, P]) of
+    one dtype; gamma, beta float32 [channels] or None. Returns out."""
+    lib = load_library()
+    batch, channels = y.shape[0], y.shape[1]
+    P = y.numel() // max(1, batch * channels)
+    if y.dim() < 3 or batch * channels * P != y.numel():
+        raise ValueError(f"y shape {tuple(y.shape)} is not [batch, channels, ...]")
+    for t, nm in ((z, "z"), (out, "out")):
+        if t is not None and (tuple(t.shape) != tuple(y.shape) or t.dtype != y.dtype):
+            raise ValueError(f"{nm} must have the shape and dtype of y")
+    for t, nm in ((gamma, "gamma"), (beta, "beta")):
+        if t is not None and t.numel() != channels:
+            raise ValueError(f"{nm} must have {channels} elements")
+    _check(lib.vmb_ss2d_out_norm(_dev(y, "y"), _dev(z, "z"), _f32(gamma, "gamma"),
+                                 _f32(beta, "beta"), float(eps), _dev(out, "out"), batch,
+                                 channels, P, _dtype(y, "y"), _stream(stream)),
+           "vmb_ss2d_out_norm")
+    return out
 
 
 def vmb_discrete_scan(abar: torch.Tensor, bu: torch.Tensor, C: torch.Tensor,

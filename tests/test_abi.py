@@ -4,6 +4,7 @@ launching anything (the pointers below are never dereferenced)."""
 import ctypes
 
 import pytest
+import torch
 
 from paper_2412_16602_amd import vmb
 
@@ -37,6 +38,19 @@ def test_version_and_status_strings(lib):
     for s in range(9):
         assert lib.vmb_status_string(s)
     assert lib.vmb_status_string(OK) == b"ok"
+
+
+# A call that passes validation goes on to launch its kernels. With the fake
+# addresses below that is harmless only on a host without a GPU, where the
+# launch fails (VMB_ERR_HIP) and the status shows that validation let the call
+# through; on a GPU host such calls are skipped.
+NO_GPU = torch.cuda.device_count() == 0
+
+
+def passes(call):
+    """Assert that ``call()`` passes validation (only run without a GPU)."""
+    if NO_GPU:
+        assert call() in (OK, 8)
 
 
 # fake, well-separated, 256-aligned "device" addresses
@@ -89,15 +103,12 @@ def test_mean_options_rules(lib):
     for name, val in (("VMB_MEAN_SKIP_PER_CHANNEL", SKIP1), ("VMB_MEAN_RAW", RAW),
                       ("VMB_MEAN_NO_BROADCAST", NOBC), ("VMB_MEAN_POOLED", POOL)):
         assert f"{name} = {val}" in text
-    # a call that passes validation reaches the launch, which fails on a host
-    # without a GPU (VMB_ERR_HIP): the status says validation let it through
-    passed = (OK, 8)
     for opt in (0, SKIP1, RAW, NOBC, SKIP1 | RAW, RAW | NOBC):
-        assert scan_call(lib, ex, options=opt) in passed
+        passes(lambda: scan_call(lib, ex, options=opt))
     assert scan_call(lib, ex, options=32) == UNSUP
     # the pooled reading only on its own, in either layout
-    assert scan_call(lib, ex, options=POOL) in passed
-    assert scan_call(lib, ex, options=POOL, layout=TWO_D) in passed
+    passes(lambda: scan_call(lib, ex, options=POOL))
+    passes(lambda: scan_call(lib, ex, options=POOL, layout=TWO_D))
     for other in (SKIP1, RAW, NOBC):
         assert scan_call(lib, ex, options=POOL | other) == UNSUP
     assert scan_call(lib, ex, options=NOBC | SKIP1) == UNSUP
@@ -105,21 +116,21 @@ def test_mean_options_rules(lib):
     ZOH = vmb.VMB_SCAN_ZOH
     assert "VMB_SCAN_ZOH = 16" in text and ZOH == 16
     for opt in (ZOH, ZOH | SKIP1, ZOH | NOBC):
-        assert scan_call(lib, ex, options=opt) in passed
+        passes(lambda: scan_call(lib, ex, options=opt))
     for opt in (ZOH | RAW, ZOH | POOL):
         assert scan_call(lib, ex, options=opt) == UNSUP
     full = "vmb_selective_scan_fwd_ex"
-    assert scan_call(lib, full, options=0) in passed
-    assert scan_call(lib, full, options=ZOH) in passed
-    assert scan_call(lib, full, options=ZOH, layout=TWO_D) in passed
+    passes(lambda: scan_call(lib, full, options=0))
+    passes(lambda: scan_call(lib, full, options=ZOH))
+    passes(lambda: scan_call(lib, full, options=ZOH, layout=TWO_D))
     for opt in (SKIP1, RAW, NOBC, POOL, 32):
         assert scan_call(lib, full, options=opt) == UNSUP
     assert scan_call(lib, ex, options=NOBC, layout=TWO_D) == UNSUP
-    assert scan_call(lib, ex, options=SKIP1 | RAW, layout=TWO_D) in passed
+    passes(lambda: scan_call(lib, ex, options=SKIP1 | RAW, layout=TWO_D))
     # without the broadcast y holds batch*K*L elements: [P(7), +4*12*4 B) overlaps
     # nothing here, and y placed just past the end of u (4*8*12 floats) is fine
-    assert scan_call(lib, ex, options=NOBC, y=P(0, 4 * 8 * 12 * 4)) in passed
-    assert scan_call(lib, ex, options=0, y=P(0, 4 * 8 * 12 * 4)) in passed
+    passes(lambda: scan_call(lib, ex, options=NOBC, y=P(0, 4 * 8 * 12 * 4)))
+    passes(lambda: scan_call(lib, ex, options=0, y=P(0, 4 * 8 * 12 * 4)))
     assert scan_call(lib, ex, options=NOBC, y=P(0, 4 * 8 * 12 * 4 - 16)) == ALIAS
 
 
@@ -188,6 +199,51 @@ def test_channel_mean_rejects(lib):
     assert f(P(0), P(1), 0, 3, 8, None) == SHAPE and f(P(0), P(1), 2, 3, 0, None) == SHAPE
     assert f(P(0, 4), P(1), 2, 3, 8, None) == ALIGN and f(P(0), P(1, 8), 2, 3, 8, None) == ALIGN
     assert f(P(0), P(0, 128), 2, 3, 8, None) == ALIAS
+
+
+def test_projections_rejects(lib):
+    f = lib.vmb_ss2d_projections
+    # u, delta: [1, 4, 8, 12]; W [4, 2 + 8, 8]; W_dt [4, 8, 2]; B, C [1, 4, 4, 12]; R = 2, N = 4
+    ok = dict(u=P(0), W=P(1), Wd=P(2), d=P(3), B=P(4), C=P(5), b=1, K=4, ch=8, L=12, N=4, R=2,
+              dt=F32)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["u"], a["W"], a["Wd"], a["d"], a["B"], a["C"], a["b"], a["K"], a["ch"], a["L"],
+                 a["N"], a["R"], a["dt"], None)
+
+    passes(call)
+    assert call(u=None) == NULL and call(W=None) == NULL and call(C=None) == NULL
+    assert call(b=0) == SHAPE and call(R=0) == SHAPE and call(L=0) == SHAPE
+    assert call(dt=3) == DTYPE
+    assert call(N=3) == UNSUP and call(R=65) == UNSUP and call(Wd=None) == UNSUP
+    passes(lambda: call(Wd=None, R=1))  # the broadcast form
+    assert call(u=P(0, 8)) == ALIGN and call(W=P(1, 2)) == ALIGN and call(B=P(4, 4)) == ALIGN
+    assert call(d=P(0, 64)) == ALIAS and call(B=P(1)) == ALIAS and call(C=P(4, 16)) == ALIAS
+
+
+def test_out_norm_rejects(lib):
+    f = lib.vmb_ss2d_out_norm
+    # y, z, out: [2, 8, 12] floats (768 B); gamma, beta [8]
+    ok = dict(y=P(0), z=P(1), g=P(2), be=P(3), eps=1e-5, o=P(4), b=2, ch=8, p=12, dt=F32)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["y"], a["z"], a["g"], a["be"], a["eps"], a["o"], a["b"], a["ch"], a["p"],
+                 a["dt"], None)
+
+    passes(call)
+    assert call(y=None) == NULL and call(o=None) == NULL
+    passes(lambda: call(z=None, g=None, be=None))  # all optional
+    assert call(b=0) == SHAPE and call(ch=0) == SHAPE and call(p=-1) == SHAPE
+    assert call(eps=-1.0) == SHAPE and call(eps=float("nan")) == SHAPE
+    assert call(eps=float("inf")) == SHAPE
+    assert call(dt=9) == DTYPE
+    assert call(y=P(0, 2)) == ALIGN and call(g=P(2, 2)) == ALIGN
+    passes(lambda: call(y=P(0, 2), o=P(4, 2), z=None, dt=BF16))  # bf16: 2-byte alignment
+    assert call(o=P(0, 512)) == ALIAS and call(o=P(1)) == ALIAS and call(o=P(2, 4)) == ALIAS
 
 
 def test_python_binding_refuses_cpu_tensors():
