@@ -12,7 +12,9 @@
 // flattened pixels and its 1024 threads are PX pixels x 1024 / PX channel
 // groups (channel d belongs to group d % groups), so every load covers PX
 // consecutive pixels of 64 / PX channel rows: PX = 16 for fp32 and 32 for
-// bf16 (64-byte row segments either way). A thread loads all of its
+// bf16 (64-byte row segments either way), halved down to a quarter while the
+// grid has fewer than 512 workgroups and every thread keeps four channels
+// (short maps: 7x7 at batch 32 has 1568 pixels of 1536 channels). A thread loads all of its
 // channels' y and z at once into registers (up to J = 32 each), so the whole
 // tensor is in flight and HBM is read once; the mean and the centred sum of
 // squares (exact in fp32 for any offset of the mean) are then formed from
@@ -166,11 +168,27 @@ vmb_status launch_out_norm(const void* y, const void* z, const float* gamma, con
                            float eps, void* out, int64_t batch, int64_t channels, int64_t P,
                            vmb_dtype dt, hipStream_t s) {
     const int64_t pixels = batch * P;
-    if ((pixels + 15) / 16 > int64_t{0x7fffffff}) return VMB_ERR_UNSUPPORTED;
-    if (dt == VMB_F32)
-        launch_t<float, 16>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
-    else
-        launch_t<bf16_t, 32>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+    if ((pixels + 3) / 4 > int64_t{0x7fffffff}) return VMB_ERR_UNSUPPORTED;
+    // widest tile (64-byte row segments) whose grid has 512 workgroups, as
+    // long as every thread keeps at least four channels (the group sums are
+    // added serially, so idle groups cost)
+    auto shrink = [&](int px) {
+        int k = 0;
+        while (k < 2 && (pixels + px - 1) / px < 512 && channels >= 4 * (kThreads / (px / 2)))
+            px /= 2, ++k;
+        return px;
+    };
+    if (dt == VMB_F32) {
+        const int px = shrink(16);
+        if (px == 16) launch_t<float, 16>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+        else if (px == 8) launch_t<float, 8>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+        else launch_t<float, 4>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+    } else {
+        const int px = shrink(32);
+        if (px == 32) launch_t<bf16_t, 32>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+        else if (px == 16) launch_t<bf16_t, 16>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+        else launch_t<bf16_t, 8>(channels, s, y, z, gamma, beta, eps, out, int(P), pixels);
+    }
     return check_launch();
 }
 

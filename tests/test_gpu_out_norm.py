@@ -41,6 +41,11 @@ CASES = [  # batch, channels, pixels
     ("b3_c70_p45", 3, 70, 45),       # 135 pixels: tiles straddle images
     ("b2_c17_p1", 2, 17, 1),         # one pixel per image
     ("b5_c1_p20", 5, 1, 20),         # one channel: zero variance, out = beta
+    # tile widths: 16 pixels from 8192 pixels or with few channels, 8 from
+    # 4096 pixels (and 512 channels), 4 below (and 1024 channels)
+    ("tile16_b2_c40_p4500", 2, 40, 4500),
+    ("tile8_b1_c600_p5000", 1, 600, 5000),
+    ("tile4_b3_c1100_p300", 3, 1100, 300),
 ]
 
 
@@ -75,12 +80,14 @@ def test_out_norm_no_affine_eps0():
     assert_close(got, ref, **FP32_TOL, what="no affine")
 
 
-def test_out_norm_bf16():
-    log("out norm bf16")
-    rng = np.random.default_rng(7)
-    y = rng.standard_normal((2, 96, 196))
-    z = rng.standard_normal((2, 96, 196))
-    g = (1 + 0.1 * rng.standard_normal(96)).astype(np.float32)
+# tiles 32 (16384 pixels), 16 (few channels), 8 (2048 channels, 392 pixels)
+@pytest.mark.parametrize("b,c,p", [(2, 96, 196), (1, 24, 9000), (4, 24, 4100), (2, 2048, 196)])
+def test_out_norm_bf16(b, c, p):
+    log(f"out norm bf16 {b}x{c}x{p}")
+    rng = np.random.default_rng(7 + p)
+    y = rng.standard_normal((b, c, p))
+    z = rng.standard_normal((b, c, p))
+    g = (1 + 0.1 * rng.standard_normal(c)).astype(np.float32)
     got, ref = run(y, z, g, None, 1e-5, dtype="bf16")
     assert_close(got, ref, **BF16_TOL, what="bf16")
 
