@@ -32,6 +32,14 @@
 //      R + 2N rows (MB 16-row blocks) of its column block over its slice, and
 //      the slices are summed through LDS. B and C rows leave from the
 //      accumulators; the R timescale rows go to LDS.
+//      bf16 inputs take the bf16 matrix cores (v_mfma_f32_16x16x16_bf16): u
+//      is exact in bf16, W is split into bf16 hi + lo parts (hi the rounded
+//      W, lo the rounded remainder), and the two products per row block
+//      are exact in fp32, so W is carried to about 2^-17 of itself (far
+//      below the bf16 rounding of the outputs) at eight times the fp32
+//      matrix rate. u is staged transposed ([position][channel]) and W as
+//      [row][channel], so each lane's four consecutive channels are one
+//      8-byte LDS read.
 //   2. delta: W_dt is staged in LDS 64 channels at a time (a contiguous
 //      block); each wave takes one 16-channel row block of the chunk and all
 //      column blocks, K = R in steps of 4.
@@ -49,9 +57,25 @@ constexpr int kMaxR = 64;         // timescale rank at most
 constexpr int kPadR = kMaxR + 1;  // LDS row stride of the W_dt chunk
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+constexpr int kStrideB = kDC + 4;  // bf16 LDS row stride (elements): 8-byte aligned rows
 
 __device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// D += A B with A 16 x 16 (rows x K) and B 16 x 16 (K x columns) in bf16:
+// lane l holds A[l % 16][4 (l / 16) .. + 3] and B[4 (l / 16) .. + 3][l % 16]
+__device__ __forceinline__ f32x4 mfma16x16x16bf16(s16x4 a, s16x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ unsigned short bf16_bits(float x) {
+    const bf16_t h = from_f32<bf16_t>(x);
+    return *reinterpret_cast<const unsigned short*>(&h);
+}
+__device__ __forceinline__ float bf16_value(unsigned short b) {
+    return __uint_as_float(static_cast<unsigned>(b) << 16);
 }
 
 // an offset the compiler cannot see through: a load at a selected offset
@@ -69,14 +93,20 @@ __global__ __launch_bounds__(256) void k_projections(
     constexpr int P = 16 * CB;   // positions per workgroup
     constexpr int PP = P + 1;    // LDS row stride of the u chunk and the timescale rows
     constexpr int KS = 4 / CB;   // channel slices
-    constexpr int kUsz = kDC * PP;
-    constexpr int kWsz = 16 * MB * kPadD;
+    constexpr bool kBf = sizeof(T) == 2;  // bf16 matrix-core path
+    // staging sizes in floats: fp32 u [channel][position] and W [row][channel];
+    // bf16 u [position][channel] and W hi, lo [row][channel] (2-byte elements)
+    constexpr int kUsz = kBf ? (P * kStrideB) / 2 : kDC * PP;
+    constexpr int kWsz = kBf ? 16 * MB * kStrideB : 16 * MB * kPadD;
     constexpr int kPool = (kUsz + kWsz) > kDC * kPadR ? (kUsz + kWsz) : kDC * kPadR;
     static_assert((KS - 1) * CB * MB * 256 <= kPool, "partials fit the staging pool");
-    __shared__ float pool[kPool];     // phase 1: u chunk, W chunk, partials; phase 2: W_dt chunk
+    __shared__ __align__(16) float pool[kPool];  // phase 1: u chunk, W chunk, partials; phase 2: W_dt chunk
     __shared__ float ss[kMaxR * PP];  // timescale rows x_dbl[0 .. R)
     float* su = pool;
     float* sw = pool + kUsz;
+    unsigned short* su16 = reinterpret_cast<unsigned short*>(pool);
+    unsigned short* swh = reinterpret_cast<unsigned short*>(pool + kUsz);
+    unsigned short* swl = swh + 16 * MB * kStrideB;
 
     // XCD-contiguous tile order: workgroup i runs on XCD i % 8; XCD x takes
     // tiles [x q + min(x, rem), ...) of the K * tiles in (k, tile) order
@@ -138,20 +168,52 @@ __global__ __launch_bounds__(256) void k_projections(
     load(0);
     for (int d0 = 0; d0 < Dc; d0 += kDC) {
         __syncthreads();  // the previous chunk has been read
+        if constexpr (kBf) {
 #pragma unroll
-        for (int j = 0; j < kUL; ++j)
-            su[(ur0 + kURows * j) * PP + uc] = u_ok(d0, j) ? to_f32(pu[j]) : 0.0f;
+            for (int j = 0; j < kUL; ++j)
+                su16[uc * kStrideB + ur0 + kURows * j] =
+                    u_ok(d0, j) ? *reinterpret_cast<const unsigned short*>(&pu[j]) : 0;
 #pragma unroll
-        for (int j = 0; j < kWL; ++j) sw[(wr0 + 4 * j) * kPadD + wc] = w_ok(d0, j) ? pw[j] : 0.0f;
+            for (int j = 0; j < kWL; ++j) {
+                const float w = w_ok(d0, j) ? pw[j] : 0.0f;
+                const unsigned short hi = bf16_bits(w);
+                swh[(wr0 + 4 * j) * kStrideB + wc] = hi;
+                swl[(wr0 + 4 * j) * kStrideB + wc] = bf16_bits(w - bf16_value(hi));
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kUL; ++j)
+                su[(ur0 + kURows * j) * PP + uc] = u_ok(d0, j) ? to_f32(pu[j]) : 0.0f;
+#pragma unroll
+            for (int j = 0; j < kWL; ++j)
+                sw[(wr0 + 4 * j) * kPadD + wc] = w_ok(d0, j) ? pw[j] : 0.0f;
+        }
         __syncthreads();
         if (d0 + kDC < Dc) load(d0 + kDC);  // in flight during this chunk's products
+        if constexpr (kBf) {
 #pragma unroll
-        for (int j = 0; j < 16 / KS; ++j) {
-            const int kk = 4 * (ks + KS * j);
-            const float bval = su[(kk + kq) * PP + 16 * cb + col];
+            for (int j = 0; j < 4 / KS; ++j) {
+                const int kk = 16 * (ks + KS * j) + 4 * kq;
+                const s16x4 bv =
+                    *reinterpret_cast<const s16x4*>(&su16[(16 * cb + col) * kStrideB + kk]);
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-                acc[mb] = mfma16x16x4(sw[(16 * mb + col) * kPadD + kk + kq], bval, acc[mb]);
+                for (int mb = 0; mb < MB; ++mb) {
+                    const int wo = (16 * mb + col) * kStrideB + kk;
+                    acc[mb] = mfma16x16x16bf16(*reinterpret_cast<const s16x4*>(&swh[wo]), bv,
+                                               acc[mb]);
+                    acc[mb] = mfma16x16x16bf16(*reinterpret_cast<const s16x4*>(&swl[wo]), bv,
+                                               acc[mb]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 16 / KS; ++j) {
+                const int kk = 4 * (ks + KS * j);
+                const float bval = su[(kk + kq) * PP + 16 * cb + col];
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+                    acc[mb] = mfma16x16x4(sw[(16 * mb + col) * kPadD + kk + kq], bval, acc[mb]);
+            }
         }
     }
     if constexpr (KS > 1) {  // sum the channel slices into slice 0

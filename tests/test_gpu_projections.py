@@ -69,7 +69,7 @@ def test_projections_f32(name, batch, K, Dc, L, N, R, bcast):
     assert_close(to_f64(d), rd, **FP32_TOL, what=f"{name} delta")
 
 
-@pytest.mark.parametrize("batch,L", [(2, 200), (3, 2900)])  # tiles of 16 and of 64
+@pytest.mark.parametrize("batch,L", [(2, 200), (5, 900), (3, 2900)])  # tiles of 16, 32, 64
 def test_projections_bf16(batch, L):
     log(f"projections bf16 batch={batch} L={L}")
     u, ut = draw_u(batch, 4, 96, L, seed=3 + L, dtype="bf16")
