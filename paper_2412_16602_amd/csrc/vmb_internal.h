@@ -95,7 +95,12 @@ static_assert(kMeanTransposeMaxL == 6144, "full_ws_has_xt uses the same bound");
 struct MeanWsLayout {
     size_t scan, rmean, agg, carry, ytil, xt, flags, gpart, total;
 };
-inline bool mean_transposes(int64_t L, bool two_d) { return two_d && L <= kMeanTransposeMaxL; }
+// Short planes (a few cache lines) are gathered directly instead: the copy
+// pass costs more than it saves there.
+constexpr int64_t kMeanTransposeMinL = 256;
+inline bool mean_transposes(int64_t L, bool two_d) {
+    return two_d && L >= kMeanTransposeMinL && L <= kMeanTransposeMaxL;
+}
 inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, int64_t L,
                                    int64_t N, bool two_d) {
     auto up = [](size_t v) { return (v + 255) & ~size_t{255}; };
