@@ -359,6 +359,45 @@ void launch_merge_tpp(const Tin* in, Tout* out, int64_t planes, int c, int h, in
                            c, h, w, np);
 }
 
+// Planes of fewer than 128 pixels (7x7 maps) span a couple of cache lines:
+// one thread per output pixel gathers its four directions straight from
+// them (same association as above), with no LDS pass and every lane busy
+// (the plane kernel leaves part of its 64 lanes idle on 49 pixels and, with
+// L % 4 != 0, loads element by element).
+constexpr int kSmallPlane = 128;
+
+template <typename Tin, typename Tout>
+__global__ __launch_bounds__(256) void k_cross_merge_small(const Tin* __restrict__ ys,
+                                                           Tout* __restrict__ y, int Dc, int H,
+                                                           int W, int64_t total) {
+    const int64_t f = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (f >= total) return;
+    const int L = H * W;
+    const int64_t plane = f / L;
+    const int p = static_cast<int>(f - plane * L);
+    const int64_t b = plane / Dc, d = plane - b * Dc;
+    const int h = p / W, w = p - h * W;
+    const int q = w * H + h;  // the pixel's position in the column-major directions
+    const size_t seq = static_cast<size_t>(L);
+    const Tin* in0 = ys + (static_cast<size_t>(b) * 4 * Dc + d) * seq;
+    const Tin* in1 = in0 + static_cast<size_t>(Dc) * seq;
+    const Tin* in2 = in1 + static_cast<size_t>(Dc) * seq;
+    const Tin* in3 = in2 + static_cast<size_t>(Dc) * seq;
+    const float s02 = to_f32(in0[p]) + to_f32(in2[L - 1 - p]);
+    const float s13 = to_f32(in1[q]) + to_f32(in3[L - 1 - q]);
+    y[f] = from_f32<Tout>(s02 + s13);
+}
+
+template <typename Tin, typename Tout>
+void launch_merge_small(const void* ys, void* y, int64_t batch, int64_t channels, int64_t H,
+                        int64_t W, hipStream_t s) {
+    const int64_t total = batch * channels * H * W;
+    hipLaunchKernelGGL((k_cross_merge_small<Tin, Tout>),
+                       dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s,
+                       static_cast<const Tin*>(ys), static_cast<Tout*>(y), int(channels), int(H),
+                       int(W), total);
+}
+
 template <typename Tin, typename Tout>
 void launch_merge_plane(const void* ys, void* y, int64_t batch, int64_t channels, int64_t H,
                         int64_t W, hipStream_t s) {
@@ -376,6 +415,17 @@ void launch_merge_plane(const void* ys, void* y, int64_t batch, int64_t channels
 vmb_status launch_cross_merge(const void* ys, void* y, int64_t batch, int64_t channels,
                               int64_t H, int64_t W, vmb_dtype in_dt, vmb_dtype out_dt,
                               hipStream_t s) {
+    if (H * W < kSmallPlane && (batch * channels * H * W + 255) / 256 <= int64_t{0x7fffffff}) {
+        if (in_dt == VMB_F32 && out_dt == VMB_F32)
+            launch_merge_small<float, float>(ys, y, batch, channels, H, W, s);
+        else if (in_dt == VMB_F32 && out_dt == VMB_BF16)
+            launch_merge_small<float, bf16_t>(ys, y, batch, channels, H, W, s);
+        else if (in_dt == VMB_BF16 && out_dt == VMB_BF16)
+            launch_merge_small<bf16_t, bf16_t>(ys, y, batch, channels, H, W, s);
+        else
+            return VMB_ERR_DTYPE;
+        return check_launch();
+    }
     if (plane_fits(batch, channels, H, W)) {
         if (in_dt == VMB_F32 && out_dt == VMB_F32)
             launch_merge_plane<float, float>(ys, y, batch, channels, H, W, s);
