@@ -359,6 +359,8 @@ void launch_merge_tpp(const Tin* in, Tout* out, int64_t planes, int c, int h, in
                            c, h, w, np);
 }
 
+namespace {
+
 // Planes of fewer than 128 pixels (7x7 maps) span a couple of cache lines:
 // one thread per output pixel gathers its four directions straight from
 // them (same association as above), with no LDS pass and every lane busy
@@ -397,6 +399,8 @@ void launch_merge_small(const void* ys, void* y, int64_t batch, int64_t channels
                        static_cast<const Tin*>(ys), static_cast<Tout*>(y), int(channels), int(H),
                        int(W), total);
 }
+
+}  // namespace
 
 template <typename Tin, typename Tout>
 void launch_merge_plane(const void* ys, void* y, int64_t batch, int64_t channels, int64_t H,
