@@ -252,3 +252,28 @@ def test_python_binding_refuses_cpu_tensors():
     xs = torch.zeros(1, 4, 2, 12)
     with pytest.raises(ValueError):
         vmb.vmb_cross_scan(x, xs)
+
+
+def test_python_binding_checks_new_entry_points():
+    """Shape and dtype checks of the projection and norm bindings raise
+    before any device work (CPU tensors, no GPU needed)."""
+    import torch
+    y = torch.zeros(2, 8, 12)
+    with pytest.raises(ValueError):  # out of another shape
+        vmb.vmb_ss2d_out_norm(y, None, None, None, 1e-5, torch.zeros(2, 8, 11))
+    with pytest.raises(ValueError):  # gamma of the wrong length
+        vmb.vmb_ss2d_out_norm(y, None, torch.ones(7), None, 1e-5, torch.zeros_like(y))
+    with pytest.raises(ValueError):  # z of another dtype
+        vmb.vmb_ss2d_out_norm(y, torch.zeros(2, 8, 12, dtype=torch.bfloat16), None, None, 1e-5,
+                              torch.zeros_like(y))
+    u = torch.zeros(1, 4, 8, 12)
+    B = torch.zeros(1, 4, 4, 12)
+    with pytest.raises(ValueError):  # W rows != R + 2N for the N of B
+        vmb.vmb_ss2d_projections(u, torch.zeros(4, 9, 7), None, torch.zeros_like(u), B,
+                                 torch.zeros_like(B))
+    with pytest.raises(ValueError):  # W_dt of the wrong rank
+        vmb.vmb_ss2d_projections(u, torch.zeros(4, 10, 8), torch.zeros(4, 8, 3),
+                                 torch.zeros_like(u), B, torch.zeros_like(B))
+    with pytest.raises(ValueError):  # C of another shape
+        vmb.vmb_ss2d_projections(u, torch.zeros(4, 10, 8), torch.zeros(4, 8, 2),
+                                 torch.zeros_like(u), B, torch.zeros(1, 4, 4, 11))
