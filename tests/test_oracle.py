@@ -302,6 +302,37 @@ def test_mean_raw_is_full_scan_of_averaged_inputs():
     np.testing.assert_allclose(y, np.broadcast_to(ref, y.shape), rtol=2e-5, atol=2e-6)
 
 
+def test_mean_raw_softplus_averages_the_timescales():
+    """Mean before discretisation with softplus on and delta varying over the
+    channels: T averages the timescales Delta_d = softplus(delta_d + bias_d)
+    themselves (the mean of the raw Delta of eq. 6), not softplus of the mean
+    biased delta. The reduced scan is then the full scan of one channel fed
+    that mean timescale as delta, with softplus off and no bias, the mean u and
+    the mean A; D is shared over a direction's channels, so mean(D u) = D mean(u).
+    The other order of softplus and mean is checked to fail the same comparison,
+    so this pin tells the two readings apart."""
+    K, Dc, N, L = 2, 6, 3, 13
+    c = rand_case(49, batch=2, K=K, Dc=Dc, L=L, N=N, softplus=True)
+    c["delta"] = (2.0 * c["delta"]).astype(np.float32)  # spread over softplus' curved part
+    D = c["D"].reshape(K, Dc)
+    D[...] = D[:, :1]
+    y = run_mean(c, options=RAW)
+    avg = lambda a, axis: a.astype(np.float64).mean(axis=axis, keepdims=True)
+    v = c["delta"].astype(np.float64) + c["dt_bias"].astype(np.float64).reshape(1, K, Dc, 1)
+    assert np.ptp(v, axis=2).min() > 0.5  # the channels really differ
+
+    def one_channel(timescale):
+        one = dict(u=avg(c["u"], 2).astype(np.float32), delta=timescale.astype(np.float32),
+                   A=avg(c["A"].reshape(K, Dc, N), 1).reshape(K, N).astype(np.float32),
+                   B=c["B"], C=c["C"], D=D[:, 0].copy(), dt_bias=None, softplus=False)
+        return np.broadcast_to(run_full(one), y.shape)
+
+    ref = one_channel(np.logaddexp(0.0, v).mean(axis=2, keepdims=True))
+    np.testing.assert_allclose(y, ref, rtol=2e-5, atol=2e-6)
+    wrong = one_channel(np.logaddexp(0.0, v.mean(axis=2, keepdims=True)))
+    assert np.max(np.abs(wrong - y) - (2e-6 + 2e-5 * np.abs(y))) > 1e-3
+
+
 def test_mean_raw_equals_discretised_mean_when_timescale_shared():
     """If Delta and A do not vary over channels, exp(Delta A) is the same for
     every channel and mean(Delta u) = Delta mean(u): both readings of T give
