@@ -29,8 +29,11 @@
  *  - Outputs must not overlap any input (VMB_ERR_ALIAS); in-place is not
  *    supported.
  *  - Non-finite inputs are not checked; they propagate.
- *  - The library is stateless and thread-safe. Results are deterministic:
- *    no floating-point atomics, fixed summation orders.
+ *  - The library keeps no per-call state and is thread-safe. Its only
+ *    host-side state is a process-wide 64-bit counter (atomic) that gives
+ *    each mean-scan call a distinct tag for the flags its workgroups
+ *    exchange, and per-device occupancy figures read once. Results are
+ *    deterministic: no floating-point atomics, fixed summation orders.
  *  - Sizes are int64_t; a tensor may hold up to 2^31 - 1 elements per
  *    [.., L] sequence row and 2^40 elements in total.
  */
@@ -44,7 +47,7 @@
 extern "C" {
 #endif
 
-#define VMB_ABI_VERSION 1
+#define VMB_ABI_VERSION 2
 
 typedef void* vmb_stream_t; /* a hipStream_t */
 
@@ -57,7 +60,9 @@ typedef enum {
     VMB_ERR_ALIAS = 5,       /* an output overlaps an input                        */
     VMB_ERR_UNSUPPORTED = 6, /* valid but unsupported (e.g. N not in {1,2,4,8,16}) */
     VMB_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than required            */
-    VMB_ERR_HIP = 8          /* the HIP runtime reported an error at launch        */
+    VMB_ERR_HIP = 8,         /* the HIP runtime reported an error at launch        */
+    VMB_ERR_INCOMPLETE = 9   /* vmb_mean_scan_status only: a bounded wait of the
+                                call gave up; the outputs it covers are NaN      */
 } vmb_status;
 
 typedef enum {
@@ -219,7 +224,14 @@ typedef enum {
      * one scan per batch element, broadcast to every (k, d); in the 2D layout
      * the four directions' (identical) sequences are merged as usual. Only as
      * the sole option bit. */
-    VMB_MEAN_POOLED = 8
+    VMB_MEAN_POOLED = 8,
+    /* Test hook of the error report (vmb_mean_scan_status), not a reading:
+     * on the one-launch path (every sequence at most 64 chunks of 64
+     * positions, and a small grid) the first chunk of each sequence does not
+     * raise its flag and the other chunks poll at most 8 times, so each of
+     * them gives up and leaves NaN outputs; every kernel still ends normally.
+     * Calls that take the separate passes ignore it. */
+    VMB_MEAN_TEST_GIVE_UP = 1 << 30
 } vmb_mean_option;
 
 /*
@@ -239,6 +251,28 @@ vmb_status vmb_mean_scan_fwd_ex(const void* u, const void* delta, const float* A
                                 vmb_dtype out_dtype, vmb_layout layout, int64_t H, int64_t W,
                                 void* workspace, size_t workspace_bytes, unsigned options,
                                 vmb_stream_t stream);
+
+/*
+ * Completion report of the most recent vmb_mean_scan_fwd / _ex call that used
+ * `workspace` (the same pointer that call received). With at most 64 chunks
+ * of 64 positions per sequence and a small grid, the mean scan runs in one
+ * launch in which each workgroup waits for the chunk aggregates of the
+ * earlier chunks of its sequence (the carry of the chunked scan of eq. 3,
+ * composed associatively as in Appendix A). Those waits are bounded
+ * (65,536 polls); a workgroup that gives up does not use aggregates it has
+ * not seen: it writes NaN to the outputs of its chunk (every channel, and in
+ * the 2-D layout every pixel fed by them) and records the call's tag in the
+ * workspace. This call waits for `stream` (hipStreamSynchronize), reads the
+ * 24-byte record at the start of the workspace, and returns
+ *   VMB_OK             the call completed, no wait gave up;
+ *   VMB_ERR_INCOMPLETE a wait of that call gave up (outputs partly NaN);
+ *   VMB_ERR_WORKSPACE  no mean-scan call is recorded in this workspace;
+ *   VMB_ERR_NULL / VMB_ERR_ALIGN (workspace NULL / not 16-byte aligned);
+ *   VMB_ERR_HIP        the stream or the copy reported an error.
+ * The record is written by every path of the mean scan (one launch or
+ * separate passes), so a later call on the same workspace replaces it.
+ */
+vmb_status vmb_mean_scan_status(const void* workspace, vmb_stream_t stream);
 
 /*
  * One-state scan on materialised, discretised inputs: the decomposition of

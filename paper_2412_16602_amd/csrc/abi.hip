@@ -1,6 +1,6 @@
 // abi.hip -- extern "C" entry points of libvmb: validate on the host, then
-// enqueue the kernels on the caller's stream. Nothing here synchronises,
-// allocates, prints or throws.
+// enqueue the kernels on the caller's stream. Nothing here allocates, prints
+// or throws; only vmb_mean_scan_status synchronises (it reads a result back).
 #include "vmb_internal.h"
 
 using namespace vmb;
@@ -160,6 +160,12 @@ vmb_status vmb_channel_mean(const float* x, float* xm, int64_t batch, int64_t ch
     return launch_channel_mean(x, xm, batch, channels, L, static_cast<hipStream_t>(stream));
 }
 
+vmb_status vmb_mean_scan_status(const void* workspace, vmb_stream_t stream) {
+    if (!workspace) return VMB_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0) return VMB_ERR_ALIGN;
+    return mean_scan_status(workspace, static_cast<hipStream_t>(stream));
+}
+
 const char* vmb_status_string(vmb_status s) {
     switch (s) {
         case VMB_OK: return "ok";
@@ -171,6 +177,7 @@ const char* vmb_status_string(vmb_status s) {
         case VMB_ERR_UNSUPPORTED: return "valid but unsupported configuration";
         case VMB_ERR_WORKSPACE: return "workspace missing or too small";
         case VMB_ERR_HIP: return "HIP runtime error at launch";
+        case VMB_ERR_INCOMPLETE: return "a bounded wait of the call gave up; its outputs are partly NaN";
         default: return "unknown status";
     }
 }

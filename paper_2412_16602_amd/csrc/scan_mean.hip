@@ -32,7 +32,9 @@
 // All sums run in a fixed order, so results are deterministic.
 #include <atomic>
 #include <chrono>
+#include <mutex>
 #include <random>
+#include <vector>
 
 #include "vmb_internal.h"
 
@@ -385,6 +387,16 @@ __device__ __forceinline__ void scan_chunk(const float (*part)[(part_rows<N, kRa
     }
 }
 
+// The first workgroup of the call's first mean kernel records the call's tag
+// in the workspace's completion record (word 0, and its complement in word 2,
+// so that no fill pattern reads as a recorded call).
+__device__ __forceinline__ void record_call(const MeanStatus& st) {
+    if (threadIdx.x == 0 && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
+        __hip_atomic_store(st.words, st.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(st.words + 2, ~st.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 // With groups == 1 the reduce scans its chunk itself; otherwise each of the
 // groups workgroups of a chunk stores its channel group's sums (its waves
 // added in wave order) for k_mean_combine.
@@ -393,9 +405,10 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
-    int softplus, int groups) {
+    int softplus, int groups, MeanStatus st) {
     constexpr int kRows = part_rows<N, kRaw, kZoh>();
     __shared__ __align__(16) float part[kRedWaves][kRows][kC];
+    record_call(st);
     reduce_partials<N, Tin, kTwoD, kRaw, kZoh>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
                                                softplus, groups);
     __syncthreads();
@@ -469,9 +482,19 @@ __global__ __launch_bounds__(kWave) void k_mean_carry(MeanWs ws, int N, int nchu
 // Workgroups wait only on lower-numbered workgroups of their own sequence
 // (chunk is the fastest grid dimension), which are dispatched no later, so
 // the lowest unfinished workgroup never waits; every wait is also bounded
-// by a spin limit, so the kernel ends whatever happens.
+// by a spin limit, so the kernel ends whatever happens. A workgroup whose
+// wait gives up does not read aggregates it has not seen announced: it
+// records the call's failure in the workspace (word 1 of the completion
+// record) and stores NaN for its chunk, so the caller finds out from
+// vmb_mean_scan_status and no stale value is ever passed off as a result.
 constexpr int kSpinLimit = 1 << 16;
-constexpr long long kFusedMaxGrid = 2048;
+constexpr int kTestSpinLimit = 8;  // VMB_MEAN_TEST_GIVE_UP
+// Grid bound of the one-launch path, in rounds of co-resident workgroups:
+// progress does not depend on co-residency (a workgroup waits only on
+// lower-numbered ones, dispatched no later), but beyond a few rounds the
+// waiting workgroups hold compute units that the separate passes keep busy
+// (batch 128 at 56x56: 1.42 ms fused against 1.21 ms in three passes).
+constexpr int kFusedRounds = 8;
 
 // (a, b) pairs exchanged between workgroups: 64-bit device-scope atomic
 // accesses, coherent across the chip's L2 caches without cache-wide
@@ -494,12 +517,16 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
     const float* __restrict__ dt_bias, const Tin* __restrict__ xt, MeanWs ws,
-    unsigned long long* __restrict__ flags, unsigned long long epoch, Tout* __restrict__ y, int K,
-    int Dc, int L, int H, int W, int nchunks, int softplus, StoreOpts so) {
+    unsigned long long* __restrict__ flags, MeanStatus st, int spin_limit, int withhold,
+    Tout* __restrict__ y, int K, int Dc, int L, int H, int W, int nchunks, int softplus,
+    StoreOpts so) {
     static_assert(N <= kRedWaves, "one state per wave");
     __shared__ __align__(16) float part[kRedWaves][N + 2 + int(kRaw)][kC];
     __shared__ float yst[kRedWaves][kC];  // C h of state n at each position
     __shared__ float rsh[kC];             // r_mean at each position
+    __shared__ int gave_up;
+    const unsigned long long epoch = st.epoch;
+    record_call(st);
     reduce_partials<N, Tin, kTwoD, kRaw>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, kC,
                                          softplus);
     __syncthreads();
@@ -538,22 +565,32 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     // the flag is stored
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0)
+    if (threadIdx.x == 0 && !(withhold && chunk == 0))
         __hip_atomic_store(flags + bk * nchunks + chunk, epoch, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     // wait for the earlier chunks (lanes = chunks) of this sequence
-    if (wv == 0 && chunk > 0) {
+    if (wv == 0) {
         bool ready = lane >= chunk;
-        for (int spin = 0; spin < kSpinLimit; ++spin) {
+        for (int spin = 0; spin < spin_limit; ++spin) {
             if (!ready)
                 ready = __hip_atomic_load(flags + bk * nchunks + lane, __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT) == epoch;
             if (__all(ready)) break;
             __builtin_amdgcn_s_sleep(2);
         }
+        const bool failed = !__all(ready);
+        if (lane == 0) {
+            gave_up = failed ? 1 : 0;
+            if (failed)
+                __hip_atomic_store(st.words + 1, epoch ^ kFailTag, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
     __syncthreads();
-    if (wv < N) {
+    if (gave_up) {
+        // the state entering this chunk is unknown: NaN outputs, no stale sums
+        if (wv < N) yst[wv][lane] = __builtin_nanf("");
+    } else if (wv < N) {
         const int n = wv;
         // state entering this chunk: scan of the earlier chunks' aggregates
         // (device-coherent loads, issued after the flags were seen)
@@ -748,6 +785,45 @@ unsigned long long next_epoch() {
     return e ? e : counter.fetch_add(2, std::memory_order_relaxed);
 }
 
+// The completion record of this call: the workspace base and a fresh tag.
+MeanStatus call_status(const ScanArgs& a) {
+    MeanStatus st;
+    st.words = static_cast<unsigned long long*>(a.ws);
+    st.epoch = next_epoch();
+    return st;
+}
+
+// Workgroups of `kernel` (block threads each) that the current device holds
+// at once: occupancy per compute unit times the compute units, read once per
+// (kernel, device) and kept; 0 if HIP cannot say.
+long long resident_workgroups(const void* kernel, int threads) {
+    struct Entry {
+        const void* kernel;
+        int dev;
+        long long value;
+    };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        for (const Entry& e : cache)
+            if (e.kernel == kernel && e.dev == dev) return e.value;
+    }
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
+        return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    const long long v = static_cast<long long>(per_cu) * cus;
+    if (v > 0) {
+        std::lock_guard<std::mutex> lock(mu);
+        cache.push_back(Entry{kernel, dev, v});
+    }
+    return v;
+}
+
 // ---------------------------------------------------------------- pooled reading
 // T over all K * channels sequences of an image (VMB_MEAN_POOLED). The
 // reduce of the main reading gives, per (b, k) and position, the sums over
@@ -765,8 +841,10 @@ template <int N, typename Tin, bool kTwoD>
 __global__ __launch_bounds__(kC* kRedWaves) void k_pooled_sums(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const float* __restrict__ D, const float* __restrict__ dt_bias, const Tin* __restrict__ xt,
-    float* __restrict__ psum, int K, int Dc, int L, int H, int W, int C, int softplus) {
+    float* __restrict__ psum, int K, int Dc, int L, int H, int W, int C, int softplus,
+    MeanStatus st) {
     __shared__ __align__(16) float part[kRedWaves][N + 2][kC];
+    record_call(st);
     reduce_partials<N, Tin, kTwoD, false>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
                                           softplus);
     __syncthreads();
@@ -863,7 +941,7 @@ vmb_status run_pooled(const ScanArgs& a) {
                        dim3(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch)),
                        dim3(kC * kRedWaves), 0, a.stream, static_cast<const Tin*>(a.u),
                        static_cast<const Tin*>(a.delta), a.A, a.D, a.dt_bias, xt, f(lay.psum), K,
-                       Dc, L, H, W, C, a.softplus);
+                       Dc, L, H, W, C, a.softplus, call_status(a));
     vmb_status st = check_launch();
     if (st != VMB_OK) return st;
     const unsigned pblk = static_cast<unsigned>((L + 255) / 256);
@@ -919,8 +997,17 @@ vmb_status run(const ScanArgs& a) {
     // (the zero-order-hold sums need more LDS than the one-launch kernel has
     // room for next to its other buffers: those calls take the three passes)
     const int rgroups = mean_groups(a.batch, a.K, a.channels, a.L);  // reduce channel groups
-    const bool fused = !kZoh && rgroups == 1 && C == kC && nchunks <= kWave &&
-                       (nchunks == 1 || wgs <= kFusedMaxGrid);
+    bool fused = !kZoh && rgroups == 1 && C == kC && nchunks <= kWave;
+    if constexpr (!kZoh) {
+        if (fused && nchunks > 1) {
+            const long long cap = resident_workgroups(
+                reinterpret_cast<const void*>(&k_mean_fused<N, Tin, Tout, kTwoD, kRaw>),
+                kC * kRedWaves);
+            if (cap < 1) return VMB_ERR_HIP;
+            fused = wgs <= kFusedRounds * cap;
+        }
+    }
+    const MeanStatus stat = call_status(a);
     const dim3 grid(nchunks, static_cast<unsigned>(a.K), static_cast<unsigned>(a.batch));
     // 2-D layout: column-major copies of the planes first, so that every
     // direction's reduce reads stay coalesced
@@ -939,8 +1026,10 @@ vmb_status run(const ScanArgs& a) {
                            0, a.stream, static_cast<const Tin*>(a.u),
                            static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
                            static_cast<const Tin*>(a.C), a.D, a.dt_bias, xt, ws,
-                           reinterpret_cast<unsigned long long*>(p + lay.flags), next_epoch(),
-                           static_cast<Tout*>(a.y), K, Dc, L, H, W, nchunks, a.softplus, so);
+                           reinterpret_cast<unsigned long long*>(p + lay.flags), stat,
+                           (a.options & VMB_MEAN_TEST_GIVE_UP) ? kTestSpinLimit : kSpinLimit,
+                           (a.options & VMB_MEAN_TEST_GIVE_UP) ? 1 : 0, static_cast<Tout*>(a.y),
+                           K, Dc, L, H, W, nchunks, a.softplus, so);
         const vmb_status sf = check_launch();
         if (sf != VMB_OK || !kTwoD) return sf;
         return launch_merge_broadcast<Tin, Tout>(ws.ytil, a);
@@ -950,7 +1039,7 @@ vmb_status run(const ScanArgs& a) {
                        dim3(kC * kRedWaves), 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), a.D, a.dt_bias, xt, ws, K, Dc, L, H, W, C,
-                       nchunks, a.softplus, rgroups);
+                       nchunks, a.softplus, rgroups, stat);
     vmb_status st = check_launch();
     if (st != VMB_OK) return st;
     if (rgroups > 1) {
@@ -1009,6 +1098,15 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 }
 
 }  // namespace
+
+vmb_status mean_scan_status(const void* ws, hipStream_t s) {
+    if (hipStreamSynchronize(s) != hipSuccess) return VMB_ERR_HIP;
+    unsigned long long rec[3] = {0, 0, 0};
+    if (hipMemcpy(rec, ws, sizeof(rec), hipMemcpyDeviceToHost) != hipSuccess) return VMB_ERR_HIP;
+    // tags are odd and stored with their complement: otherwise no call is recorded
+    if ((rec[0] & 1ull) == 0 || rec[2] != ~rec[0]) return VMB_ERR_WORKSPACE;
+    return rec[1] == (rec[0] ^ kFailTag) ? VMB_ERR_INCOMPLETE : VMB_OK;
+}
 
 vmb_status launch_mean_scan(const ScanArgs& a) {
     if (a.batch > 65535 || a.K > 65535) return VMB_ERR_UNSUPPORTED;

@@ -78,8 +78,21 @@ inline int mean_groups(int64_t batch, int64_t K, int64_t channels, int64_t L) {
     return g > 1 ? static_cast<int>(g) : 1;
 }
 
+// Completion record at the start of every mean-scan workspace (both
+// readings' layouts), 64-bit words: word 0 holds the tag (epoch, odd) of the
+// last call that used the workspace and word 2 its complement, so that no fill
+// pattern reads as a recorded call; word 1 holds the tag of the last call whose
+// bounded wait gave up, XORed with kFailTag.
+constexpr size_t kMeanStatusBytes = 256;
+constexpr unsigned long long kFailTag = 0x9e3779b97f4a7c15ull;
+struct MeanStatus {
+    unsigned long long* words;  // workspace base
+    unsigned long long epoch;   // this call's tag (odd)
+};
+
 // Byte offsets of the mean variant's workspace regions (each 256-byte
 // aligned), for bk = batch * K direction sequences of L positions:
+//   status                    : the completion record above
 //   scan  [bk][N][L][2] float : chunk-local inclusive scan (P, H)
 //   rmean [bk][L]       float : channel mean of D * u
 //   agg   [bk][nch][N][2]     : chunk aggregates
@@ -108,7 +121,7 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, i
     const int chunk = mean_chunk(batch, K, L);
     const size_t nch = static_cast<size_t>((L + chunk - 1) / chunk);
     MeanWsLayout o;
-    o.scan = 0;
+    o.scan = kMeanStatusBytes;
     o.rmean = o.scan + up(bk * N * L * 2 * 4);
     o.agg = o.rmean + up(bk * L * 4);
     o.carry = o.agg + up(bk * nch * N * 2 * 4);
@@ -131,6 +144,7 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, i
 //   rbar  [batch][L]   : pooled skip term
 //   ytil  [batch][4][L]: ytilde written once per direction (2-D merge input)
 //   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL, as in the main reading
+// after the completion record (kMeanStatusBytes).
 struct PooledWsLayout {
     size_t psum, abar, bu, cbar, h, ones, rbar, ytil, xt, total;
 };
@@ -140,7 +154,7 @@ inline PooledWsLayout pooled_ws_layout(int64_t batch, int64_t K, int64_t channel
     const size_t bk = static_cast<size_t>(batch) * static_cast<size_t>(K);
     const size_t b = static_cast<size_t>(batch), l = static_cast<size_t>(L), n = static_cast<size_t>(N);
     PooledWsLayout o;
-    o.psum = 0;
+    o.psum = kMeanStatusBytes;
     o.abar = o.psum + up(bk * (n + 2) * l * 4);
     o.bu = o.abar + up(b * n * l * 4);
     o.cbar = o.bu + up(b * n * l * 4);
@@ -217,6 +231,8 @@ inline size_t full_ws_xt_bytes(int64_t batch, int64_t channels, int64_t L) {
     return (static_cast<size_t>(batch) * channels * L * 4 + 255) & ~size_t{255};
 }
 vmb_status launch_mean_scan(const ScanArgs& a);
+// Reads the completion record of a mean-scan workspace (synchronises the stream).
+vmb_status mean_scan_status(const void* ws, hipStream_t s);
 
 inline vmb_status check_launch() {
     return hipGetLastError() == hipSuccess ? VMB_OK : VMB_ERR_HIP;

@@ -179,7 +179,7 @@ vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
     }
     if (!supported_n(a.N)) return VMB_ERR_UNSUPPORTED;
     const unsigned known = VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST |
-                           VMB_MEAN_POOLED | VMB_SCAN_ZOH;
+                           VMB_MEAN_POOLED | VMB_SCAN_ZOH | VMB_MEAN_TEST_GIVE_UP;
     if (a.options & ~known) return VMB_ERR_UNSUPPORTED;
     if (!mean_variant && (a.options & ~static_cast<unsigned>(VMB_SCAN_ZOH))) return VMB_ERR_UNSUPPORTED;
     if ((a.options & VMB_MEAN_POOLED) && a.options != VMB_MEAN_POOLED) return VMB_ERR_UNSUPPORTED;

@@ -24,12 +24,15 @@ VMB_F32, VMB_BF16 = 0, 1
 VMB_LAYOUT_SEQ, VMB_LAYOUT_2D = 0, 1
 # vmb_mean_option bits (vmb_mean_scan_fwd_ex)
 VMB_MEAN_SKIP_PER_CHANNEL, VMB_MEAN_RAW, VMB_MEAN_NO_BROADCAST, VMB_MEAN_POOLED = 1, 2, 4, 8
+# test hook of the mean scan's error report (see include/vmb.h)
+VMB_MEAN_TEST_GIVE_UP = 1 << 30
 # vmb_scan_option bits (vmb_selective_scan_fwd_ex; vmb_mean_scan_fwd_ex takes them too)
 VMB_SCAN_ZOH = 16
 
 STATUS = {0: "VMB_OK", 1: "VMB_ERR_NULL", 2: "VMB_ERR_SHAPE", 3: "VMB_ERR_DTYPE",
           4: "VMB_ERR_ALIGN", 5: "VMB_ERR_ALIAS", 6: "VMB_ERR_UNSUPPORTED",
-          7: "VMB_ERR_WORKSPACE", 8: "VMB_ERR_HIP"}
+          7: "VMB_ERR_WORKSPACE", 8: "VMB_ERR_HIP", 9: "VMB_ERR_INCOMPLETE"}
+VMB_OK, VMB_ERR_WORKSPACE, VMB_ERR_INCOMPLETE = 0, 7, 9
 
 
 class VmbError(RuntimeError):
@@ -75,6 +78,8 @@ def load_library():
     lib.vmb_channel_mean.restype = I
     lib.vmb_scan_workspace_bytes.argtypes = [I, I64, I64, I64, I64, I64, I]
     lib.vmb_scan_workspace_bytes.restype = ctypes.c_size_t
+    lib.vmb_mean_scan_status.argtypes = [P, P]
+    lib.vmb_mean_scan_status.restype = I
     lib.vmb_status_string.argtypes = [I]
     lib.vmb_status_string.restype = ctypes.c_char_p
     lib.vmb_abi_version.argtypes = []
@@ -208,14 +213,16 @@ def _scan(name, mean_variant, u, delta, A, B, C, D, dt_bias, delta_softplus, y, 
     for t, nm in ((D, "D"), (dt_bias, "dt_bias")):
         if t is not None and t.numel() != K * channels:
             raise ValueError(f"{nm} must hold K * channels = {K * channels} values")
-    if workspace is None:
-        need = vmb_scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout)
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=delta.device) if need else None
-    ws_ptr = _dev(workspace, "workspace")
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     args = [_dev(u, "u"), _dev(delta, "delta"), _f32(A, "A"), _dev(B, "B"), _dev(C, "C"),
             _f32(D, "D"), _f32(dt_bias, "dt_bias"), int(bool(delta_softplus)), _dev(y, "y"),
-            batch, K, channels, L, N, in_dt, out_dt, layout, H, W, ws_ptr, ws_bytes]
+            batch, K, channels, L, N, in_dt, out_dt, layout, H, W]
+    if workspace is not False:  # False: the entry point takes no workspace
+        if workspace is None:
+            need = vmb_scan_workspace_bytes(mean_variant, batch, K, channels, L, N, layout)
+            workspace = (torch.empty(max(need, 1), dtype=torch.uint8, device=delta.device)
+                         if need else None)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        args += [_dev(workspace, "workspace"), ws_bytes]
     if options is not None:
         args.append(int(options))
     status = getattr(lib, name)(*args, _stream(stream))
@@ -250,6 +257,18 @@ def vmb_mean_scan_fwd_ex(u, delta, A, B, C, D, dt_bias, delta_softplus, y, optio
     y is [batch, K, 1, L] with VMB_MEAN_NO_BROADCAST). Returns y."""
     return _scan("vmb_mean_scan_fwd_ex", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
                  y, layout, workspace, stream, options=options)
+
+
+def vmb_mean_scan_status(workspace: torch.Tensor, stream=None) -> int:
+    """Completion status of the last mean-scan call that used ``workspace``
+    (waits for the stream): VMB_OK, VMB_ERR_INCOMPLETE (a bounded wait gave up,
+    outputs partly NaN) or VMB_ERR_WORKSPACE (no call recorded). Returns the
+    code; other codes raise."""
+    status = int(load_library().vmb_mean_scan_status(_dev(workspace, "workspace"),
+                                                     _stream(stream)))
+    if status not in (VMB_OK, VMB_ERR_WORKSPACE, VMB_ERR_INCOMPLETE):
+        raise VmbError(status, "vmb_mean_scan_status")
+    return status
 
 
 def vmb_ss2d_projections(u: torch.Tensor, W: torch.Tensor, W_dt: Optional[torch.Tensor],

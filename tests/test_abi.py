@@ -34,10 +34,22 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert vmb.abi_version() == 1
-    for s in range(9):
-        assert lib.vmb_status_string(s)
+    assert vmb.abi_version() == 2
+    for s in range(10):
+        assert lib.vmb_status_string(s) != b"unknown status"
     assert lib.vmb_status_string(OK) == b"ok"
+    assert lib.vmb_status_string(10) == b"unknown status"
+
+
+def test_mean_status_rejects(lib):
+    # validation before any HIP call: NULL and misaligned workspaces
+    assert lib.vmb_mean_scan_status(None, None) == NULL
+    assert lib.vmb_mean_scan_status(ctypes.c_void_p(BASE + 8), None) == ALIGN
+    with open(vmb.HEADER_PATH) as f:
+        text = f.read()
+    assert "VMB_ERR_INCOMPLETE = 9" in text and vmb.VMB_ERR_INCOMPLETE == 9
+    assert "VMB_MEAN_TEST_GIVE_UP = 1 << 30" in text
+    assert vmb.VMB_MEAN_TEST_GIVE_UP == 1 << 30
 
 
 # A call that passes validation goes on to launch its kernels. With the fake
@@ -105,6 +117,12 @@ def test_mean_options_rules(lib):
         assert f"{name} = {val}" in text
     for opt in (0, SKIP1, RAW, NOBC, SKIP1 | RAW, RAW | NOBC):
         passes(lambda: scan_call(lib, ex, options=opt))
+    # the test hook of the error report goes with every reading but the pooled one
+    GIVE = vmb.VMB_MEAN_TEST_GIVE_UP
+    for opt in (GIVE, GIVE | SKIP1, GIVE | RAW):
+        passes(lambda: scan_call(lib, ex, options=opt))
+    assert scan_call(lib, ex, options=GIVE | POOL) == UNSUP
+    assert scan_call(lib, "vmb_selective_scan_fwd_ex", options=GIVE) == UNSUP
     assert scan_call(lib, ex, options=32) == UNSUP
     # the pooled reading only on its own, in either layout
     passes(lambda: scan_call(lib, ex, options=POOL))

@@ -4,7 +4,8 @@ sequence waiting on the flags of the earlier chunks).
 The flags live in the caller's workspace, so the results must not depend on
 what the workspace held before the call (zeros, all-ones bytes, random bytes,
 the flags of an earlier call), and repeated calls must agree bit for bit.
-Grids on both sides of the single-launch limit (2048 workgroups) are checked
+Grids on both sides of the single-launch limit (eight rounds of co-resident
+workgroups: 2048 with one 1024-thread workgroup per compute unit) are checked
 against the oracle, so the one-launch and the three-pass paths are both
 covered at the same sequence length."""
 import numpy as np
@@ -70,3 +71,79 @@ def test_fused_fewer_states(N):
     ref = oracle_seq(inp, "mean", "seq")
     assert_close(got, ref, **FP32_TOL, what=f"mean N={N}")
     assert np.all(np.isfinite(got))
+
+
+# ---------------------------------------------------------------- error report
+# The one-launch path's waits are bounded. VMB_MEAN_TEST_GIVE_UP makes them
+# give up from the host side: the first chunk of every sequence withholds its
+# flag and the others poll 8 times, so every kernel still ends normally. A
+# chunk that gives up must not pass stale aggregates off as results: its
+# outputs are NaN and vmb_mean_scan_status reports the call as incomplete.
+
+def _stage1_like(batch=1, channels=8, seed=41):
+    # 49 chunks of 64 positions per sequence: the one-launch path
+    return workloads.custom_shape(batch, 56, 56, channels, 16, "f32", seed, True)
+
+
+@pytest.mark.parametrize("fill", ["zeros", "ones"])
+def test_status_of_unused_workspace(fill):
+    log(f"mean status unused workspace={fill}")
+    ws = _workspace(_stage1_like(), fill)
+    torch.cuda.synchronize()
+    assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_ERR_WORKSPACE
+
+
+def test_give_up_is_reported_and_poisons_only_the_unfinished_chunks():
+    log("mean give-up (sequence layout)")
+    shp = _stage1_like()
+    inp = workloads.make_inputs(shp, "seq")
+    ref = oracle_seq(inp, "mean", "seq")
+    ws = _workspace(shp, "random")
+    y = to_f64(run_scan(inp, "mean", "seq", workspace=ws, options=vmb.VMB_MEAN_TEST_GIVE_UP))
+    assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_ERR_INCOMPLETE
+    # chunk 0 of every sequence waits for nothing and is exact; every later
+    # chunk gave up and is NaN in every channel
+    assert_close(y[..., :64], ref[..., :64], **FP32_TOL, what="chunk 0 after give-up")
+    assert np.all(np.isnan(y[..., 64:])), "chunks after a give-up must be NaN"
+    # the next ordinary call on the same workspace completes and says so
+    again = to_f64(run_scan(inp, "mean", "seq", workspace=ws))
+    assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_OK
+    assert_close(again, ref, **FP32_TOL, what="mean after a give-up call")
+
+
+def test_give_up_2d_layout():
+    log("mean give-up (2-D layout)")
+    shp = _stage1_like(seed=42)
+    inp = workloads.make_inputs(shp, "2d")
+    need = vmb.vmb_scan_workspace_bytes(1, 1, 4, shp.channels, shp.L, 16, vmb.VMB_LAYOUT_2D)
+    ws = torch.zeros(need, dtype=torch.uint8, device=dev())
+    y = to_f64(run_scan(inp, "mean", "2d", workspace=ws, options=vmb.VMB_MEAN_TEST_GIVE_UP))
+    assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_ERR_INCOMPLETE
+    # every pixel of a 56x56 map lies past position 63 in some direction
+    assert np.all(np.isnan(y))
+    ok = to_f64(run_scan(inp, "mean", "2d", workspace=ws))
+    assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_OK
+    assert np.all(np.isfinite(ok))
+
+
+@pytest.mark.parametrize("case", ["three_pass_long", "zoh", "pooled"])
+def test_status_of_other_paths(case):
+    # the separate passes never wait; they record the call all the same, so
+    # a give-up left by an earlier call on the workspace is not reported again
+    log(f"mean status {case}")
+    if case == "three_pass_long":
+        shp = workloads.custom_shape(1, 1, 64 * 70, 8, 16, "f32", 43, True)  # 70 chunks
+        opts = vmb.VMB_MEAN_TEST_GIVE_UP  # ignored off the one-launch path
+    else:
+        shp = _stage1_like(seed=44)
+        opts = vmb.VMB_SCAN_ZOH if case == "zoh" else vmb.VMB_MEAN_POOLED
+    inp = workloads.make_inputs(shp, "seq")
+    ws = _workspace(shp, "zeros")
+    if case != "three_pass_long":
+        fail_shp = _stage1_like(seed=45)
+        run_scan(workloads.make_inputs(fail_shp, "seq"), "mean", "seq", workspace=ws,
+                 options=vmb.VMB_MEAN_TEST_GIVE_UP)
+        assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_ERR_INCOMPLETE
+    y = to_f64(run_scan(inp, "mean", "seq", workspace=ws, options=opts))
+    assert vmb.vmb_mean_scan_status(ws) == vmb.VMB_OK
+    assert np.all(np.isfinite(y))
