@@ -253,6 +253,32 @@ vmb_status vmb_mean_scan_fwd_ex(const void* u, const void* delta, const float* A
                                 vmb_stream_t stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid hipMalloc): the VMeanba
+ * scan of vmb_mean_scan_fwd (same arguments, same kernels, same results)
+ * without the workspace arguments. Its scratch space is a fixed 8 MiB device
+ * array inside the library, one per GPU, held until the process ends; the
+ * call allocates nothing. Shapes whose workspace
+ * (vmb_scan_workspace_bytes(1, ...)) exceeds 8 MiB return VMB_ERR_WORKSPACE
+ * (the 56x56 map with 192 channels at batch 1 needs about 1.7 MB in the SEQ
+ * layout, 4.3 MB in the 2D layout). Every call on one GPU shares that GPU's
+ * array: calls that overlap in time on one GPU (different streams, or several
+ * host threads) race and must be serialised by the caller. Nothing in the
+ * array needs clearing between calls. The completion record of the array is
+ * not exposed (vmb_mean_scan_status needs a workspace pointer): a bounded
+ * wait that gives up still leaves NaN outputs, never stale values.
+ * Errors as for vmb_mean_scan_fwd, plus VMB_ERR_HIP if the array's device
+ * address cannot be read.
+ */
+vmb_status vmb_mean_scan_fwd_noalloc(const void* u, const void* delta, const float* A,
+                                     const void* B, const void* C, const float* D,
+                                     const float* dt_bias, int delta_softplus, void* y,
+                                     int64_t batch, int64_t K, int64_t channels, int64_t L,
+                                     int64_t N, vmb_dtype in_dtype, vmb_dtype out_dtype,
+                                     vmb_layout layout, int64_t H, int64_t W,
+                                     vmb_stream_t stream);
+
+/*
  * Completion report of the most recent vmb_mean_scan_fwd / _ex call that used
  * `workspace` (the same pointer that call received). With at most 64 chunks
  * of 64 positions per sequence and a small grid, the mean scan runs in one

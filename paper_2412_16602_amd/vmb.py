@@ -78,6 +78,8 @@ def load_library():
     lib.vmb_channel_mean.restype = I
     lib.vmb_scan_workspace_bytes.argtypes = [I, I64, I64, I64, I64, I64, I]
     lib.vmb_scan_workspace_bytes.restype = ctypes.c_size_t
+    lib.vmb_mean_scan_fwd_noalloc.argtypes = scan[:-3] + [P]
+    lib.vmb_mean_scan_fwd_noalloc.restype = I
     lib.vmb_mean_scan_status.argtypes = [P, P]
     lib.vmb_mean_scan_status.restype = I
     lib.vmb_status_string.argtypes = [I]
@@ -257,6 +259,14 @@ def vmb_mean_scan_fwd_ex(u, delta, A, B, C, D, dt_bias, delta_softplus, y, optio
     y is [batch, K, 1, L] with VMB_MEAN_NO_BROADCAST). Returns y."""
     return _scan("vmb_mean_scan_fwd_ex", True, u, delta, A, B, C, D, dt_bias, delta_softplus,
                  y, layout, workspace, stream, options=options)
+
+
+def vmb_mean_scan_fwd_noalloc(u, delta, A, B, C, D, dt_bias, delta_softplus, y,
+                              layout: int = VMB_LAYOUT_SEQ, stream=None):
+    """VMeanba scan without a workspace argument (the library's fixed 8 MiB
+    per-device scratch array; calls overlapping on one GPU race). Returns y."""
+    return _scan("vmb_mean_scan_fwd_noalloc", True, u, delta, A, B, C, D, dt_bias,
+                 delta_softplus, y, layout, False, stream)
 
 
 def vmb_mean_scan_status(workspace: torch.Tensor, stream=None) -> int:
