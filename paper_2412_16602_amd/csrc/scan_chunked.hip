@@ -46,37 +46,6 @@ __device__ __forceinline__ float dpp(float old, float v) {
                                                                  kRowMask, 0xf, false));
 }
 
-// Inclusive scan of (P, H) over the 64 lanes of the wave, in lane order,
-// (plain asm: no side effects, so the scheduler may interleave other work)
-// combine (P1, H1) then (P2, H2) -> (P1 P2, P2 H1 + H2). Each step reads the
-// partner lane's values through DPP inside the arithmetic (v_fmac / v_mul
-// with a DPP source); a lane whose partner does not exist is not written,
-// which is the identity. Wait states: a VALU result read through DPP needs
-// two independent instructions (or s_nop) in between.
-__device__ __forceinline__ void wave_scan(float& P, float& Hs) {
-    asm(
-        "s_nop 1\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-        "s_nop 1\n"
-        : "+v"(Hs), "+v"(P));
-}
-
 // T consecutive elements starting at p (element-aligned). full: all T are
 // in range; otherwise only the first cnt are read, the rest become 0.
 template <int T>

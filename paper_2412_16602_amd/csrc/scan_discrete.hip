@@ -37,32 +37,6 @@ __device__ __forceinline__ float dpp(float old, float v) {
                                                                  kRowMask, 0xf, false));
 }
 
-// Inclusive scan of (P, H) over the 64 lanes in lane order; a lane without a
-// partner keeps its value (the identity). DPP reads of a VALU result need two
-// independent instructions or s_nop in between.
-__device__ __forceinline__ void lane_scan(float& P, float& H) {
-    asm("s_nop 1\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-        "s_nop 1\n"
-        : "+v"(H), "+v"(P));
-}
-
 // kRun values starting at element p of a row: two 16-byte loads when the row
 // is 16-byte aligned and the run lies inside it, else element loads of the
 // first cnt (the rest 0).
@@ -175,7 +149,7 @@ __global__ __launch_bounds__(kWave* kScanWaves) void k_discrete_scan(
             H = __builtin_fmaf(a[i], H, x[i]);
             P *= a[i];
         }
-        lane_scan(P, H);
+        wave_scan(P, H);
         // exclusive prefix: lane - 1's inclusive value, (1, 0) on lane 0
         const float Pex = dpp<0x138, 0xf>(1.0f, P);
         const float Hex = dpp<0x138, 0xf>(0.0f, H);
@@ -242,7 +216,7 @@ __global__ __launch_bounds__(kWave* kSplitMaxWaves) void k_discrete_scan_split(
             H = __builtin_fmaf(a[i], H, x[i]);
             P *= a[i];
         }
-        lane_scan(P, H);
+        wave_scan(P, H);
         const float Pex = dpp<0x138, 0xf>(1.0f, P);
         const float Hex = dpp<0x138, 0xf>(0.0f, H);
         if (lane == kWave - 1) {

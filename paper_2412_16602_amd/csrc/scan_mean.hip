@@ -49,31 +49,6 @@ constexpr int kAhead = 4;       // channels of delta / u in flight per wave
 __device__ float g_zero = 0.0f;  // stands in for an absent dt_bias / D (never written)
 constexpr int kFinWaves = 4;    // waves of a finish workgroup
 
-// Inclusive scan over the 64 lanes of the (a, b) pairs, in lane order
-// (lanes without a partner are left unchanged: identity).
-__device__ __forceinline__ void wave_scan(float& a, float& b) {
-    asm("s_nop 1\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-        "s_nop 1\n"
-        : "+v"(b), "+v"(a));
-}
-
 // Workspace layout, per (batch, k) = bk, for L positions and nch chunks:
 //   scan[bk][n][t][2] : chunk-local inclusive (P, H) of state n at position t
 //   rmean[bk][t]      : r_mean

@@ -25,36 +25,6 @@ constexpr int kShortWaves = 8;
 constexpr int kShortThreads = kShortWaves * kWave;
 constexpr int kWaveShr1 = 0x138;  // DPP wave_shr:1 (GFX9 encoding)
 
-// Inclusive scan of (P, H) over segments of S lanes (S = 16 or 32), in lane
-// order. DPP row shifts stay inside a row of 16 lanes, so rows are natural
-// segments; for S = 32 the row broadcast joins rows 0-1 and 2-3. A lane
-// without a partner is left unchanged (the identity). Wait states: a VALU
-// result read through DPP needs two independent instructions (or s_nop).
-template <int S>
-__device__ __forceinline__ void seg_scan(float& P, float& Hs) {
-    static_assert(S == 16 || S == 32, "segments of 16 or 32 lanes");
-    asm("s_nop 1\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 0\n"
-        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-        "s_nop 1\n"
-        : "+v"(Hs), "+v"(P));
-    if constexpr (S == 32) {
-        asm("v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-            "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-            "s_nop 1\n"
-            : "+v"(Hs), "+v"(P));
-    }
-}
-
 __device__ __forceinline__ float shr1(float old, float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
                                                                  __builtin_bit_cast(int, v),

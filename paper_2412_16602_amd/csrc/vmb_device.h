@@ -53,13 +53,14 @@ __device__ __forceinline__ float log1p_unit(float e) {
     return s * p;
 }
 
-// Timescale of eq. 6: softplus(v) = max(v, 0) + log(1 + exp(-|v|)), or v
-// itself when the softplus flag is off.
-__device__ __forceinline__ float timescale(float v, bool softplus) {
-    if (!softplus) return v;
+// softplus(v) = max(v, 0) + log(1 + exp(-|v|)), the timescale map of eq. 6.
+__device__ __forceinline__ float softplus(float v) {
     const float e = fast_exp2(-__builtin_fabsf(v) * kLog2e);
     return __builtin_fmaxf(v, 0.0f) + log1p_unit(e);
 }
+
+// Timescale of eq. 6: softplus(v), or v itself when the softplus flag is off.
+__device__ __forceinline__ float timescale(float v, bool sp) { return sp ? softplus(v) : v; }
 
 // Zero-order-hold coefficient of B (eq. 4, second line read as
 // (Delta A)^-1 (exp(Delta A) - I) Delta B): Bbar u = q * B with
@@ -87,6 +88,74 @@ __device__ __forceinline__ int pixel_of(int k, int t, int H, int W) {
     const int w = tt / H;
     const int h = tt - w * H;
     return h * W + w;
+}
+
+}  // namespace vmb
+
+namespace vmb {
+
+// ---------------------------------------------------------------- DPP scans
+// Inclusive scans over the lanes of a wave of the pair combine of the
+// linear recurrence (Appendix A: the associative scan of eq. 3),
+//   (P1, H1) then (P2, H2) -> (P1 P2, P2 H1 + H2),
+// in lane order. Each level reads the partner lane through DPP inside the
+// arithmetic (v_fmac / v_mul with a DPP source operand); a lane whose partner
+// does not exist is not written, which is the identity. Wait states: a VALU
+// result read through DPP needs two independent instructions (or s_nop) in
+// between. Plain asm (no side effects): the scheduler may move other work
+// around it.
+
+// One pair over all 64 lanes (row shifts 1, 2, 4, 8, then the row
+// broadcasts of lanes 15 and 31).
+__device__ __forceinline__ void wave_scan(float& P, float& Hs) {
+    asm("s_nop 1\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+        "s_nop 1\n"
+        : "+v"(Hs), "+v"(P));
+}
+
+// One pair over segments of S lanes (S = 16 or 32): DPP row shifts stay
+// inside a row of 16 lanes, so rows are natural segments; for S = 32 the
+// broadcast of lane 15 joins rows 0-1 and 2-3 (row mask 0xa).
+template <int S>
+__device__ __forceinline__ void seg_scan(float& P, float& Hs) {
+    static_assert(S == 16 || S == 32, "segments of 16 or 32 lanes");
+    asm("s_nop 1\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 0\n"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "v_mul_f32_dpp %1, %1, %1 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+        "s_nop 1\n"
+        : "+v"(Hs), "+v"(P));
+    if constexpr (S == 32) {
+        asm("v_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+            "v_mul_f32_dpp %1, %1, %1 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+            "s_nop 1\n"
+            : "+v"(Hs), "+v"(P));
+    }
 }
 
 }  // namespace vmb
