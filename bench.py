@@ -15,14 +15,17 @@ Cache), so every step streams from HBM.
 
 Prints one JSON line (rank 0). The `roofline` object covers the dominant
 kernel, the full scan, timed alone on the sequence layout with HIP events on
-its stream. Its arithmetic floor (one exp and five other VALU slots per
-(channel, state, position)) lies above its HBM floor, so it is reported as
-ALU-bound: 7 FLOP per element against the 45.9 TFLOP/s this instruction mix
-can reach (256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz non-packed fp32 issue, exp at
-half rate); the HBM fraction is reported next to it. `traffic` is the HBM
-bytes per launch measured with rocprofv3 counters (profiles/), reported only
-while the kernel source still matches the one profiled. `cpu_baseline` times
-the fp64 oracle on the host.
+its stream, against the published MI355X peaks: HBM 8 TB/s (algorithmic bytes:
+u, delta, B, C read once, y written once) and fp32 vector 157.3 TFLOP/s (7 FLOP
+per (channel, state, position): Delta*A, exp, Delta*u*B, state FMA, output
+FMA). `bound` names the roof the kernel comes closer to; the other one is
+reported next to it. `traffic` is the HBM bytes per launch measured with
+rocprofv3 counters (profiles/), reported only while the kernel sources still
+match the ones profiled. `roofline.step` does the same for the whole timed
+step (2-D layout: the scan and the merge). `cpu_baseline` times the fp64
+oracle on the host (full and mean SS2D forwards, one-thread times, a sampled
+batched workload) and `accuracy` compares the GPU outputs of the timed step
+with it.
 
 --calibrate runs a plain 256 MiB device copy first, the reference dispatch the
 counter runs scale FETCH_SIZE / WRITE_SIZE by.
@@ -45,16 +48,16 @@ if ROOT not in sys.path:
 import workloads  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
-# non-packed fp32 VALU issue: 256 CUs * 4 SIMDs * 16 lanes * 2.4 GHz lane-slots/s
-VALU_SLOTS_PER_S = 256 * 4 * 16 * 2.4e9
+FP32_VECTOR_PEAK_TFLOPS = 157.3  # MI355X published fp32 vector peak (packed FMA)
 # per (channel, state, position): Delta*A, exp, Delta*u*B, state FMA, output FMA
 FLOP_PER_ELEM = 7
-SLOTS_PER_ELEM = 6  # mul, exp (2 slots: half-rate transcendental), mul, fma, fma
-ALU_PEAK_TFLOPS = VALU_SLOTS_PER_S * FLOP_PER_ELEM / SLOTS_PER_ELEM / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "full_scan_seq_56x56_c192_n16_traffic.txt")
-# the sources the profiled kernel is compiled from
+STEP_FILE = os.path.join(ROOT, "profiles", "ss2d_step_56x56_c192_n16_traffic.txt")
+# the sources the profiled kernels are compiled from
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2412_16602_amd", "csrc", f)
                   for f in ("scan_chunked.hip", "vmb_device.h")]
+STEP_SOURCES = [os.path.join(ROOT, "paper_2412_16602_amd", "csrc", f)
+                for f in ("scan_chunked.hip", "vmb_device.h", "cross.hip", "scan_full.hip")]
 METRIC = ("SS2D selective-scan µs/call + HBM GB/s (% peak), full vs mean, "
           "VMamba-T 56×56")
 ROTATE_BYTES = 768 << 20  # > 2x the 256 MB MALL
@@ -149,6 +152,7 @@ def gpu_bench(args):
                 "p90": round(float(np.percentile(t, 90)), 3)}
 
     res = {}
+    outputs = {}
     # --- the step: SS2D forward, 2-D layout, full and mean
     for variant in ("full", "mean"):
         sets, lay = make_sets(inp2d, "2d", variant, n_rot)
@@ -160,6 +164,8 @@ def gpu_bench(args):
         warm = timed(runner(variant, sets[:1], lay), args.steps, 2)
         dist = per_call(call, min(args.steps, 100))
         res[f"ss2d_{variant}"] = dict(us=us, warm_us=warm, wall_s=wall, dist=dist)
+        torch.cuda.synchronize()
+        outputs[variant] = sets[0]["y"].cpu().numpy()  # set 0: the workload's own inputs
         del sets
     # --- dominant kernel alone: the scan, sequence layout (one kernel per call for full)
     for variant in ("full", "mean"):
@@ -169,31 +175,52 @@ def gpu_bench(args):
         res[f"seq_{variant}"] = dict(us=us)
         del sets
     torch.cuda.synchronize()
-    return res, step_bytes, scan_bytes, n_rot
+    return res, step_bytes, scan_bytes, n_rot, outputs
 
 
-def source_hash() -> str:
+def source_hash(paths=None) -> str:
     import hashlib
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
+    for path in (KERNEL_SOURCES if paths is None else paths):
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per launch of the full scan from the committed counter summary
-    (lines "key: value"), or None if absent or taken on other kernel sources."""
+def profile_values(path, sources):
+    """The machine-read lines ("key: value") of a committed counter summary,
+    or None if absent or taken on other kernel sources."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             kv = dict(line.split(":", 1) for line in f if ":" in line)
     except OSError:
         return None
     kv = {k.strip(): v.strip() for k, v in kv.items()}
-    if kv.get("kernel_sources_sha256_16") != source_hash():
+    if kv.get("kernel_sources_sha256_16") != source_hash(sources):
+        return None
+    return kv
+
+
+def measured_traffic():
+    """HBM bytes per launch of the full scan from the committed counter
+    summary, or None."""
+    kv = profile_values(TRAFFIC_FILE, KERNEL_SOURCES)
+    try:
+        return int(kv["traffic_bytes_per_launch"]) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def measured_step():
+    """Kernel-trace time and counter bytes of the whole 2-D step (all its
+    kernels) from the committed summary, or None."""
+    kv = profile_values(STEP_FILE, STEP_SOURCES)
+    if not kv:
         return None
     try:
-        return int(kv["traffic_bytes_per_launch"])
+        return {"kernels_us": float(kv["step_kernels_us"]),
+                "counter_bytes": int(kv["step_traffic_bytes"]),
+                "kernels": kv.get("step_kernels", "")}
     except (KeyError, ValueError):
         return None
 
@@ -210,29 +237,77 @@ def calibrate_copy():
     del src, dst
 
 
-def cpu_baseline(budget_s: float):
-    """The fp64 oracle on the host: one SS2D forward (cross-scan, full scan,
-    merge) at the bench workload, repeated until about budget_s seconds."""
+def _timed_reps(fn, budget_s: float, max_reps: int = 1000):
+    """Run fn() until about budget_s seconds have passed; mean seconds per call."""
+    reps, total = 0, 0.0
+    while True:
+        t0 = time.perf_counter()
+        fn()
+        total += time.perf_counter() - t0
+        reps += 1
+        if total >= budget_s or reps >= max_reps:
+            return total / reps, reps
+
+
+def cpu_baseline(budget_s: float, gpu_out=None):
+    """The fp64 oracle on the host, in bounded samples (about budget_s seconds
+    each for the two main lines, less for the others):
+      - one SS2D forward (cross-scan, full scan, merge) at the bench workload,
+        every available core; this is `value`;
+      - the same forward with the mean (VMeanba) scan;
+      - one-thread full forwards of the tiny 7x7 workload and the stage-1 one;
+      - a sampled batched workload: one batch item of the batch-128 bf16
+        stage-1 workload (items are independent), scaled to the batch.
+    With gpu_out (the GPU outputs of the timed step on its first input set),
+    also the elementwise error of those outputs against the oracle."""
     import oracle
 
     threads = len(os.sched_getaffinity(0))
     threads = min(threads, int(os.environ.get("OMP_NUM_THREADS", threads)))
     inp = workloads.make_inputs(workloads.STAGE1, "2d")
     H, W = inp.shape.H, inp.shape.W
-    reps, t_total = 0, 0.0
-    while True:
-        t0 = time.perf_counter()
-        xs = oracle.cross_scan(inp.x)
-        ys = oracle.full_scan(xs, inp.delta, inp.A, inp.B, inp.C, inp.D, inp.dt_bias, True,
-                              nthreads=threads)
-        oracle.cross_merge(ys, H, W, "f64")
-        t_total += time.perf_counter() - t0
-        reps += 1
-        if t_total >= budget_s or reps >= 1000:
-            break
-    return dict(value=t_total / reps * 1e6, unit="us/call", cores=threads, kind="oracle",
-                sample=f"{reps} x one SS2D forward (cross-scan, full scan, merge) at 1x56x56, "
-                       f"192 channels, N=16, fp64", cpu_model=cpu_model())
+
+    def forward(variant, x_inp, nthreads):
+        xs = oracle.cross_scan(x_inp.x)
+        fn = oracle.full_scan if variant == "full" else oracle.mean_scan
+        ys = fn(xs, x_inp.delta, x_inp.A, x_inp.B, x_inp.C, x_inp.D, x_inp.dt_bias, True,
+                nthreads=nthreads)
+        return oracle.cross_merge(np.ascontiguousarray(ys), x_inp.shape.H, x_inp.shape.W, "f64")
+
+    full_s, full_n = _timed_reps(lambda: forward("full", inp, threads), budget_s)
+    mean_s, mean_n = _timed_reps(lambda: forward("mean", inp, threads), budget_s / 2)
+    tiny = workloads.make_inputs(workloads.TINY, "2d")
+    tiny_s, tiny_n = _timed_reps(lambda: forward("full", tiny, 1), 1.0)
+    one_s, one_n = _timed_reps(lambda: forward("full", inp, 1), budget_s / 2, max_reps=3)
+    # one batch item of the batch-128 bf16 workload, drawn with its own recipe
+    big = workloads.make_inputs(workloads.BATCHED_BF16, "2d", batch=1)
+    big_s, big_n = _timed_reps(lambda: forward("full", big, threads), budget_s / 4, max_reps=20)
+    res = dict(value=full_s * 1e6, unit="us/call", cores=threads, kind="oracle",
+               sample=f"{full_n} x one SS2D forward (cross-scan, full scan, merge) at 1x56x56, "
+                      f"192 channels, N=16, fp64, {threads} threads",
+               cpu_model=cpu_model(),
+               mean_us=round(mean_s * 1e6, 1),
+               mean_sample=f"{mean_n} x the same forward with the VMeanba mean scan",
+               single_thread_us={"tiny_7x7_c32_n4_full": round(tiny_s * 1e6, 1),
+                                 "stage1_56x56_c192_n16_full": round(one_s * 1e6, 1)},
+               batched_sample={"workload": workloads.BATCHED_BF16.name,
+                               "sample": f"{big_n} x one of 128 batch items (independent), "
+                                         f"{threads} threads",
+                               "us_per_item": round(big_s * 1e6, 1),
+                               "us_whole_batch_scaled": round(big_s * 1e6 * 128, 1)})
+    acc = None
+    if gpu_out is not None:
+        acc = {}
+        for variant in ("full", "mean"):
+            if variant not in gpu_out:
+                continue
+            ref = forward(variant, inp, threads)
+            got = np.asarray(gpu_out[variant], dtype=np.float64)
+            err = np.abs(got - ref)
+            acc[variant] = {"max_abs_err": float(err.max()),
+                            "max_rel_err": float((err / np.maximum(np.abs(ref), 1e-30)).max()),
+                            "worst_vs_fp32_tol": float((err / (1e-5 + 1e-4 * np.abs(ref))).max())}
+    return res, acc
 
 
 # The paper's Table 1 times of the original (all-channel) kernel on its own
@@ -495,7 +570,8 @@ def workloads_bench(steps: int, warmup: int):
                              "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
                              "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                              "alu_frac": round(elems * FLOP_PER_ELEM / (us * 1e-6) / 1e12
-                                               / ALU_PEAK_TFLOPS, 4) if variant == "full" else None})
+                                               / FP32_VECTOR_PEAK_TFLOPS, 4)
+                             if variant == "full" else None})
                 del ws
             del sets, y
             torch.cuda.empty_cache()
@@ -671,7 +747,7 @@ def main():
 
     if args.calibrate:
         calibrate_copy()
-    res, step_bytes, scan_bytes, n_rot = gpu_bench(args)
+    res, step_bytes, scan_bytes, n_rot, outputs = gpu_bench(args)
     full, mean = res["ss2d_full"], res["ss2d_mean"]
     sfull, smean = res["seq_full"], res["seq_mean"]
     kern_us = sfull["us"]
@@ -679,6 +755,26 @@ def main():
     shp = workloads.STAGE1
     elems = shp.batch * 4 * shp.channels * shp.N * shp.L
     achieved_tf = elems * FLOP_PER_ELEM / (kern_us * 1e-6) / 1e12
+    hbm_frac = achieved / HBM_PEAK_GBPS
+    alu_frac = achieved_tf / FP32_VECTOR_PEAK_TFLOPS
+    rows = shp.batch * 4 * shp.channels * shp.L  # position-rows of one launch
+    if hbm_frac >= alu_frac:
+        bound = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                 "unit": "GB/s", "frac": round(hbm_frac, 4)}
+        other = {"alu": {"achieved_tflops": round(achieved_tf, 3),
+                         "peak_tflops": FP32_VECTOR_PEAK_TFLOPS, "frac": round(alu_frac, 4),
+                         "flop_per_element": FLOP_PER_ELEM, "elements": elems}}
+    else:
+        bound = {"bound": "alu", "achieved": round(achieved_tf, 3),
+                 "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(alu_frac, 4)}
+        other = {"hbm": {"achieved_gbps": round(achieved, 1), "peak_gbps": HBM_PEAK_GBPS,
+                         "frac": round(hbm_frac, 4)}}
+    step_prof = measured_step()
+    step = {"us": round(full["us"], 3), "algorithmic_bytes": step_bytes,
+            "hbm_frac": round(step_bytes / (full["us"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "kernels": "full scan (2-D layout, per-direction outputs) + cross-merge",
+            "kernels_us_traced": step_prof["kernels_us"] if step_prof else None,
+            "traffic": step_prof["counter_bytes"] if step_prof else None}
     out = {
         "metric": METRIC,
         "value": round(full["us"], 3),
@@ -708,18 +804,14 @@ def main():
                      "full_gbps": round(scan_bytes / (sfull["us"] * 1e-6) / 1e9, 1),
                      "mean_gbps": round(scan_bytes / (smean["us"] * 1e-6) / 1e9, 1),
                      "mean_speedup": round(sfull["us"] / smean["us"], 3)},
-        "roofline": {"bound": "alu", "achieved": round(achieved_tf, 3),
-                     "peak": round(ALU_PEAK_TFLOPS, 2), "unit": "TFLOP/s",
-                     "frac": round(achieved_tf / ALU_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic(),
+        "roofline": {**bound, "traffic": measured_traffic(),
                      "kernel": "full scan (positions over lanes), sequence layout",
-                     "avg_us": round(kern_us, 3), "elements": elems,
-                     "flop_per_element": FLOP_PER_ELEM,
-                     "algorithmic_bytes": scan_bytes, "hbm_gbps": round(achieved, 1),
-                     "hbm_frac": round(achieved / HBM_PEAK_GBPS, 4)},
+                     "avg_us": round(kern_us, 3), "algorithmic_bytes": scan_bytes,
+                     "bytes_per_position_row": round(scan_bytes / rows, 3),
+                     "position_rows": rows, **other, "step": step},
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
+        out["cpu_baseline"], out["accuracy"] = cpu_baseline(args.cpu_budget, outputs)
     print(json.dumps(out), flush=True)
     if args.variants:
         print(json.dumps(variants_bench(args.steps, args.warmup)), flush=True)
