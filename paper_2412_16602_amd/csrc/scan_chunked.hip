@@ -248,6 +248,35 @@ __device__ __forceinline__ void stage_pieces(const Tin* src, Tin* dst, int len, 
     }
 }
 
+// One 16-byte piece per lane from global memory into LDS (gfx950
+// global_load_lds: lane i's piece lands at dst + 16 i, dst wave-uniform).
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ void lds_dma16(const void* src, void* dst) {
+    __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)dst, 16, 0, 0);
+}
+
+// Copy of len elements from src into LDS at dst by one wave, in 16-byte
+// pieces (len a multiple of the piece): pieces first, first + step, ... of
+// 64 lanes each. The wave waits for vmcnt before it reads the copy.
+template <typename Tin>
+__device__ __forceinline__ void wave_copy(const Tin* src, Tin* dst, int len, int first, int step,
+                                          int lane) {
+    constexpr int kPer = 16 / static_cast<int>(sizeof(Tin));
+    const int jl = lane * kPer;
+    for (int base = first * kWave * kPer; base < len; base += step * kWave * kPer)
+        if (base + jl < len) lds_dma16(src + base + jl, dst + base);
+}
+
+// Slot idx of size elements in the two C stage buffers viewed end to end
+// (slots never straddle the two arrays).
+template <typename Tin>
+__device__ __forceinline__ Tin* stage_slot(Tin (*a)[kStageMax], Tin (*b)[kStageMax], int idx,
+                                           int size) {
+    const int per = (2 * kStageMax) / size;
+    return idx < per ? &a[0][0] + idx * size : &b[0][0] + (idx - per) * size;
+}
+
 template <typename Tin>
 __device__ __forceinline__ void stage_row(const Tin* row, Tin* dst, int cs, int len, bool vec4,
                                           int issuer, int lane) {
@@ -288,8 +317,8 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     __shared__ float hcar[kComputeWaves][N];    // per wave: state carried into the next chunk
     // B and C slices of a pair of states, double-buffered (distinct arrays so
     // that copies into one buffer never order reads of the other)
-    __shared__ Tin bst0[2][kStageMax], bst1[2][kStageMax];
-    __shared__ Tin cst0[2][kStageMax], cst1[2][kStageMax];
+    __shared__ __align__(16) Tin bst0[2][kStageMax], bst1[2][kStageMax];
+    __shared__ __align__(16) Tin cst0[2][kStageMax], cst1[2][kStageMax];
     // per compute wave: its outputs on their way to a coalesced store
     __shared__ __align__(16) float ystage[kComputeWaves][kWave * T];
 
@@ -306,9 +335,15 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
-    const int chunk = kWv * kWave * T;
+    constexpr int chunk = kWv * kWave * T;
     const int nchunks = (L + chunk - 1) / chunk;
     const bool vec4 = (L % (16 / static_cast<int>(sizeof(Tin)))) == 0;
+    // A sequence that fits one chunk, in rows of whole 16-byte pieces, has its
+    // delta and u runs copied into LDS with coalesced pieces before the first
+    // barrier and read from there (see the compute waves' prologue).
+    const bool staged = nchunks == 1 && vec4;
+    static_assert(kComputeWaves <= 2 * ((2 * kStageMax) / (kWave * T)), "u slots per wave");
+    static_assert(G <= 2 * ((2 * kStageMax) / chunk), "plane slots per channel");
     const Tin* Bb = Bm + static_cast<size_t>(bk) * N * L;
     const Tin* Cb = Cm + static_cast<size_t>(bk) * N * L;
 
@@ -324,6 +359,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         stage(Bb, 0, 0, bst0[0]);
         stage(Bb, 0, 1, bst0[1]);
         wait_vmem();
+        if (kTwoD && staged) __syncthreads();  // pairs with the plane barrier
         __syncthreads();
         for (int p = 0; p < npairs; ++p) {
             Tin (*cdst)[kStageMax] = (p & 1) ? cst1 : cst0;
@@ -426,7 +462,45 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     };
 
     float dv0[T], uv0[T];
-    load_chunk(0, dv0, uv0);
+    if (staged) {
+        // Loaded straight from global memory, each instruction of a stride-T
+        // run load touches a cache line per lane (and in the 2-D layout the
+        // column-major directions gather across the whole plane). Instead the
+        // wave copies its delta range into its output slice and its u range
+        // (sequence layout) or a share of its channel's plane (2-D layout:
+        // every direction's positions map into the one plane) into the C
+        // stage buffers, which the copy waves first fill after the first
+        // barrier, then reads its runs from LDS (stride-T words, T odd:
+        // conflict-free).
+        const int seg0 = w * kWave * T;
+        const int n = L - seg0 < kWave * T ? (L - seg0 > 0 ? L - seg0 : 0) : kWave * T;
+        Tin* dsl = reinterpret_cast<Tin*>(ystage[wv]);
+        wave_copy(drow + seg0, dsl, n, 0, 1, lane);
+        const Tin* usl;
+        if constexpr (kTwoD) {
+            Tin* pl = stage_slot(cst0, cst1, g, chunk);
+            wave_copy(urow, pl, L, w, kWv, lane);
+            wait_vmem();
+            __syncthreads();  // the channel's plane is complete
+            usl = pl;
+        } else {
+            Tin* ul = stage_slot(cst0, cst1, wv, kWave * T);
+            wave_copy(urow + seg0, ul, n, 0, 1, lane);
+            wait_vmem();
+            usl = ul;
+        }
+        const int cnt = L - run < T ? (L - run > 0 ? L - run : 0) : T;
+#pragma unroll
+        for (int i = 0; i < T; ++i) dv0[i] = i < cnt ? to_f32(dsl[lane * T + i]) : 0.0f;
+        if constexpr (kTwoD) {
+            load_run_2d<T>(usl, k, cnt > 0 ? run : 0, H, W, L, uv0, cnt);
+        } else {
+#pragma unroll
+            for (int i = 0; i < T; ++i) uv0[i] = i < cnt ? to_f32(usl[lane * T + i]) : 0.0f;
+        }
+    } else {
+        load_chunk(0, dv0, uv0);
+    }
 
     __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
     // keep every use of the loaded values after the barrier (the compiler
