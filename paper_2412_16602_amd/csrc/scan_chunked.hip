@@ -153,15 +153,14 @@ __device__ __forceinline__ void load_run_2d(const Tin* plane, int k, int t0, int
 }
 
 // Phase 1 of one state for one lane: a_i, b_i of its run (registers), the
-// run aggregate, the inclusive scan over the wave, this wave's aggregate
-// published to xg[wv] by the last lane, and the lane's exclusive prefix
-// (Pex, Hex) kept for phase 2.
+// run aggregate, the inclusive scan over the wave (Pin, Hin, kept for phase
+// 2), and this wave's aggregate published to xg[wv] by the last lane.
 // With kZoh, Bbar u takes the zero-order-hold form (zoh_q, from the run's u
 // values uvr and inv_an = 1 / A_n) instead of Delta u.
 template <int T, typename Tin, bool kZoh = false>
 __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], const float (&du)[T],
                                              float s2, const Tin* bsrc, float (&a)[T],
-                                             float (&bu)[T], float& Pex, float& Hex,
+                                             float (&bu)[T], float& Pin, float& Hin,
                                              float (*xg)[2], int lane, int wv,
                                              const float (&uvr)[T], float inv_an) {
     float agg = 0.0f;
@@ -171,29 +170,27 @@ __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], co
         a[i] = fast_exp2(x2);
         const float q = kZoh ? zoh_q(x2, a[i], du[i], uvr[i], inv_an) : du[i];
         bu[i] = q * to_f32(bsrc[i]);
-        agg = __builtin_fmaf(a[i], agg, bu[i]);
+        agg = i == 0 ? bu[0] : __builtin_fmaf(a[i], agg, bu[i]);
     }
-    float P = fast_exp2(s2 * an);
-    float Hs = agg;
-    wave_scan(P, Hs);
+    Pin = fast_exp2(s2 * an);
+    Hin = agg;
+    wave_scan(Pin, Hin);
     if (lane == kWave - 1) {
-        xg[wv][0] = P;
-        xg[wv][1] = Hs;
+        xg[wv][0] = Pin;
+        xg[wv][1] = Hin;
     }
-    // exclusive prefix of this lane: the inclusive one of lane - 1
-    Pex = dpp<kWaveShr1, 0xf>(1.0f, P);
-    Hex = dpp<kWaveShr1, 0xf>(0.0f, Hs);
 }
 
 // Phase 2 (after the workgroup barrier): state entering this wave from the
 // channel's earlier waves and the previous chunk (*hcar, this wave's own copy
-// of the carry), then the re-walk of the run from the state entering this
-// lane, accumulating y_i += C_i h_i. Every wave of a channel composes the same
-// aggregates in the same order, so every copy of the carry into the next chunk
-// (the state leaving the channel's last wave) is the same.
+// of the carry), the state entering this lane (lane - 1's inclusive scan
+// applied to it, read across lanes), then the re-walk of the run,
+// accumulating y_i += C_i h_i. Every wave of a channel composes the same
+// aggregates in the same order, so every copy of the carry into the next
+// chunk (the state leaving the channel's last wave) is the same.
 template <int T, int kWv, typename Tin>
-__device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pex,
-                                             float Hex, const Tin* csrc, float (&yv)[T],
+__device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pin,
+                                             float Hin, const Tin* csrc, float (&yv)[T],
                                              const float (*xg)[2], float* hcar, int lane, int g,
                                              int w) {
     const float hc = *hcar;
@@ -205,7 +202,9 @@ __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&
         cnext = __builtin_fmaf(x.x, cnext, x.y);
         if (j + 1 < kWv && j + 1 == w) cin = cnext;
     }
-    float h = __builtin_fmaf(Pex, cin, Hex);
+    if (lane == 0) *hcar = cnext;
+    // lane 0 starts from cin itself (the shift leaves its old value)
+    float h = dpp<kWaveShr1, 0xf>(cin, __builtin_fmaf(Pin, cin, Hin));
 #pragma unroll
     for (int i = 0; i < T; ++i) {
         h = __builtin_fmaf(a[i], h, bu[i]);
@@ -215,7 +214,6 @@ __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&
     // next step's phase 1, which then needs two steps' run arrays at once
 #pragma unroll
     for (int i = 0; i < T; ++i) asm volatile("" : "+v"(yv[i]));
-    if (lane == 0) *hcar = cnext;
 }
 
 // Slice of the B or C row of one state copied into LDS: positions
@@ -439,15 +437,15 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
             const float2 a01 = *reinterpret_cast<const float2*>(an + n0);
             const float inv0 = kZoh ? 1.0f / a01.x : 0.0f, inv1 = kZoh ? 1.0f / a01.y : 0.0f;
             float a0[T], bu0[T], a1[T], bu1[T];
-            float Pex0, Hex0, Pex1, Hex1;
-            state_phase1<T, Tin, kZoh>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pex0, Hex0,
+            float Pin0, Hin0, Pin1, Hin1;
+            state_phase1<T, Tin, kZoh>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pin0, Hin0,
                                        xq[0], lane, wv, uv, inv0);
-            state_phase1<T, Tin, kZoh>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pex1, Hex1,
+            state_phase1<T, Tin, kZoh>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pin1, Hin1,
                                        xq[1], lane, wv, uv, inv1);
             __syncthreads();
-            state_phase2<T, kWv>(a0, bu0, Pex0, Hex0, &ccur[0][run], yv, xq[0], &hcar[wv][n0], lane,
+            state_phase2<T, kWv>(a0, bu0, Pin0, Hin0, &ccur[0][run], yv, xq[0], &hcar[wv][n0], lane,
                                  g, w);
-            state_phase2<T, kWv>(a1, bu1, Pex1, Hex1, &ccur[1][run], yv, xq[1], &hcar[wv][n0 + 1],
+            state_phase2<T, kWv>(a1, bu1, Pin1, Hin1, &ccur[1][run], yv, xq[1], &hcar[wv][n0 + 1],
                                  lane, g, w);
         };
 #pragma unroll 1
