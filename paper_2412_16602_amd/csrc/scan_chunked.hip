@@ -219,8 +219,9 @@ __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&
 // Slice of the B or C row of one state copied into LDS: positions
 // [cs, cs + len) of the row, len <= kStageMax. The copy goes straight from
 // global memory to LDS (gfx950 global_load_lds: each lane of a wave moves 16
-// or 4 bytes to LDS at base + lane * size), no registers involved. Rows whose
-// length is a multiple of 4 move 16-byte pieces, others single words. The
+// or 4 bytes to LDS at base + lane * size), no registers involved. Rows of
+// whole 16-byte pieces move 16-byte pieces, others 4-byte words (one fp32 or
+// two bf16 elements: bf16 rows reach this kernel with even lengths only). The
 // issuing wave must wait for vmcnt before the barrier that publishes them.
 constexpr int kStageMax = 4 * kWave * 13;
 constexpr int kComputeWaves = 12;  // G channels x Wv waves

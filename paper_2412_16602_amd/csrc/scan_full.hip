@@ -110,7 +110,12 @@ vmb_status dispatch_dtype(const ScanArgs& a) {
 
 }  // namespace
 
-bool use_chunked_full(const ScanArgs& a) { return a.N == 16 && a.L > kShortMaxL; }
+// The chunked kernel copies B and C rows into LDS in pieces of 4 or 16
+// bytes; a bf16 row of odd length has neither its start nor its end on a
+// 4-byte boundary, so those shapes take the lane-per-channel kernel.
+bool use_chunked_full(const ScanArgs& a) {
+    return a.N == 16 && a.L > kShortMaxL && !(a.in_dt == VMB_BF16 && (a.L & 1));
+}
 
 vmb_status launch_full_scan(const ScanArgs& a) {
     // the zero-order-hold B runs in the tile, positions-over-lanes and lane

@@ -39,10 +39,13 @@ def test_channel_group_tails(channels):
     assert_close(got, ref, **FP32_TOL, what=f"chunked channels={channels}")
 
 
+# bf16 rows of 16-byte pieces (L % 8 == 0), of 4-byte pieces (L even) and of
+# odd length (not on 4-byte boundaries: the lane-per-channel kernel takes them)
 @pytest.mark.parametrize("out", ["bf16", "f32"])
-def test_bf16(out):
-    log(f"chunked full bf16 -> {out}")
-    inp = workloads.make_inputs(shape(1, 33, 61, 6, "bf16", seed=200), "seq")
+@pytest.mark.parametrize("H,W", [(32, 64), (33, 62), (33, 61)])
+def test_bf16(out, H, W):
+    log(f"chunked full bf16 {H}x{W} -> {out}")
+    inp = workloads.make_inputs(shape(1, H, W, 6, "bf16", seed=200 + W), "seq")
     y = run_scan(inp, "full", "seq", out_dtype=torch.bfloat16 if out == "bf16" else torch.float32)
     ref = oracle_seq(inp, "full", "seq")
     assert_close(to_f64(y), ref, **(BF16_TOL if out == "bf16" else FP32_TOL), what=f"bf16->{out}")
