@@ -12,7 +12,10 @@ paper reports for the scan's activations (Section 2.1, Fig. 3): every channel
 of a position shares a N(0,1) base value plus N(0, 0.05^2) channel noise.
 
 Distributions (fixed draw order, numpy PCG64, float32 draws):
-  x or u : tiny case N(0,1); other cases base + 0.05 * noise
+  x      : tiny case N(0,1); other cases base + 0.05 * noise, [batch, channels, H, W]
+  u      : (sequence layout) x laid out in the four scan orders, [batch, K, channels, L]:
+           row by row, column by column, and both reversed (a permutation of
+           the drawn values, so both layouts see the same data)
   delta  : N(0, 0.5) (variance 0.5), shape [batch, K, channels, L]
   dt     : log-uniform in [1e-3, 1e-1] per (k, d); dt_bias = log(expm1(dt)),
            so softplus(dt_bias) = dt (the usual Mamba dt initialisation)
@@ -100,36 +103,39 @@ def _normal(rng: np.random.Generator, shape, scale: float = 1.0) -> np.ndarray:
     return out
 
 
+def scan_orders(x: np.ndarray) -> np.ndarray:
+    """A feature map [batch, channels, H, W] laid out in the four scan orders,
+    [batch, 4, channels, H*W]: row by row, column by column, then the same
+    two reversed. A permutation of x's elements (no arithmetic)."""
+    b, c, H, W = x.shape
+    rows = x.reshape(b, c, H * W)
+    cols = np.ascontiguousarray(np.swapaxes(x, 2, 3)).reshape(b, c, H * W)
+    return np.ascontiguousarray(np.stack([rows, cols, rows[..., ::-1], cols[..., ::-1]], axis=1))
+
+
 def make_inputs(shape: Shape, layout: str = "seq", *, batch: Optional[int] = None,
                 d_value: float = 1.0, seed: Optional[int] = None) -> Inputs:
     """Draw one seeded input set.
 
-    layout "seq": u is drawn directly per direction, [batch, K, channels, L].
-    layout "2d" : x is drawn as a feature map, [batch, channels, H, W].
+    The feature map x [batch, channels, H, W] is drawn for both layouts.
+    layout "2d" : x is the input.
+    layout "seq": u = x in the four scan orders, [batch, K, channels, L], is
+    the input (x is kept too). Both layouts draw the same values for a seed.
     ``batch`` overrides the shape's batch (used to draw a bounded sample of a
     large workload); ``d_value`` sets the skip vector D.
     """
+    if layout not in ("2d", "seq"):
+        raise ValueError(f"unknown layout {layout!r}")
     b = shape.batch if batch is None else batch
     s = shape.seed if seed is None else seed
     rng = np.random.Generator(np.random.PCG64(s))
     Dc, L, N, H, W = shape.channels, shape.L, shape.N, shape.H, shape.W
-    x = u = None
-    if layout == "2d":
-        if shape.low_variance:
-            base = _normal(rng, (b, 1, H, W))
-            noise = _normal(rng, (b, Dc, H, W), 0.05)
-            x = base + noise
-        else:
-            x = _normal(rng, (b, Dc, H, W))
-    elif layout == "seq":
-        if shape.low_variance:
-            base = _normal(rng, (b, K_DIRS, 1, L))
-            noise = _normal(rng, (b, K_DIRS, Dc, L), 0.05)
-            u = base + noise
-        else:
-            u = _normal(rng, (b, K_DIRS, Dc, L))
+    if shape.low_variance:
+        base = _normal(rng, (b, 1, H, W))
+        noise = _normal(rng, (b, Dc, H, W), 0.05)
+        x = base + noise
     else:
-        raise ValueError(f"unknown layout {layout!r}")
+        x = _normal(rng, (b, Dc, H, W))
     delta = _normal(rng, (b, K_DIRS, Dc, L), math.sqrt(0.5))
     lo, hi = math.log(1e-3), math.log(1e-1)
     dt = np.exp(rng.uniform(lo, hi, size=(K_DIRS * Dc,))).astype(np.float64)
@@ -141,13 +147,15 @@ def make_inputs(shape: Shape, layout: str = "seq", *, batch: Optional[int] = Non
     bits = None
     if shape.dtype == "bf16":
         bits = {}
-        if x is not None:
-            x, bits["x"] = bf16_round(x)
-        if u is not None:
-            u, bits["u"] = bf16_round(u)
+        x, bits["x"] = bf16_round(x)
         delta, bits["delta"] = bf16_round(delta)
         Bm, bits["B"] = bf16_round(Bm)
         Cm, bits["C"] = bf16_round(Cm)
+    u = None
+    if layout == "seq":
+        u = scan_orders(x)
+        if bits is not None:
+            bits["u"] = scan_orders(bits["x"])
     return Inputs(shape, x, u, np.ascontiguousarray(delta), np.ascontiguousarray(A),
                   np.ascontiguousarray(Bm), np.ascontiguousarray(Cm), Dv, dt_bias, bits)
 
