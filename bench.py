@@ -739,6 +739,9 @@ def main():
     ap.add_argument("--table1", action="store_true",
                     help="after the main line, print a second JSON line: the one-state scan "
                          "on materialised inputs at the paper's Table 1 shapes")
+    ap.add_argument("--table1-only", action="store_true",
+                    help="print only the Table 1 line (for counter runs, which serialise "
+                         "every dispatch)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this SS2D scan library runs on a single "
@@ -747,6 +750,9 @@ def main():
 
     if args.calibrate:
         calibrate_copy()
+    if args.table1_only:
+        print(json.dumps(table1_bench(max(5, args.steps // 10), 3)), flush=True)
+        return
     res, step_bytes, scan_bytes, n_rot, outputs = gpu_bench(args)
     full, mean = res["ss2d_full"], res["ss2d_mean"]
     sfull, smean = res["seq_full"], res["seq_mean"]
