@@ -20,7 +20,9 @@ namespace {
 constexpr int kTile = 32;
 constexpr int kRows = 8;  // blockDim = (kTile, kRows)
 
-template <typename T>
+// kAll = false writes only the column-major copy of each plane (direction
+// 1's sequence), to xs[plane][L].
+template <typename T, bool kAll = true>
 __global__ __launch_bounds__(kTile* kRows) void k_cross_scan(const T* __restrict__ x,
                                                              T* __restrict__ xs, int Dc, int H,
                                                              int W) {
@@ -33,7 +35,8 @@ __global__ __launch_bounds__(kTile* kRows) void k_cross_scan(const T* __restrict
     const T* src = x + static_cast<size_t>(plane) * L;
     const size_t seq = static_cast<size_t>(L);
     T* out0 = xs + (static_cast<size_t>(b) * 4 * Dc + d) * seq;  // direction 0
-    T* out1 = out0 + static_cast<size_t>(Dc) * seq;              // direction 1
+    T* out1 = kAll ? out0 + static_cast<size_t>(Dc) * seq         // direction 1
+                   : xs + static_cast<size_t>(plane) * seq;
     T* out2 = out1 + static_cast<size_t>(Dc) * seq;              // direction 2
     T* out3 = out2 + static_cast<size_t>(Dc) * seq;              // direction 3
 
@@ -45,8 +48,10 @@ __global__ __launch_bounds__(kTile* kRows) void k_cross_scan(const T* __restrict
             const int p = h * W + w;
             const T v = src[p];
             tile[r][tx] = v;
-            out0[p] = v;
-            out2[L - 1 - p] = v;
+            if constexpr (kAll) {
+                out0[p] = v;
+                out2[L - 1 - p] = v;
+            }
         }
     }
     __syncthreads();
@@ -57,7 +62,7 @@ __global__ __launch_bounds__(kTile* kRows) void k_cross_scan(const T* __restrict
             const int q = w * H + h;
             const T v = tile[tx][r];
             out1[q] = v;
-            out3[L - 1 - q] = v;
+            if constexpr (kAll) out3[L - 1 - q] = v;
         }
     }
 }
@@ -326,8 +331,20 @@ bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
 
 vmb_status launch_transpose_planes(const void* x, void* xt, int64_t batch, int64_t channels,
                                    int64_t H, int64_t W, vmb_dtype dt, hipStream_t s) {
-    if (!plane_fits(batch, channels, H, W)) return VMB_ERR_UNSUPPORTED;
-    return launch_scan_planes<false>(x, xt, batch, channels, H, W, dt, s);
+    if (plane_fits(batch, channels, H, W))
+        return launch_scan_planes<false>(x, xt, batch, channels, H, W, dt, s);
+    // planes beyond LDS: 32 x 32 tiles
+    if (!grid_fits(batch, channels, H, W)) return VMB_ERR_UNSUPPORTED;
+    const dim3 grid = tile_grid(batch, channels, H, W), block(kTile, kRows);
+    if (dt == VMB_F32)
+        hipLaunchKernelGGL((k_cross_scan<float, false>), grid, block, 0, s,
+                           static_cast<const float*>(x), static_cast<float*>(xt), int(channels),
+                           int(H), int(W));
+    else
+        hipLaunchKernelGGL((k_cross_scan<bf16_t, false>), grid, block, 0, s,
+                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(xt), int(channels),
+                           int(H), int(W));
+    return check_launch();
 }
 
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,

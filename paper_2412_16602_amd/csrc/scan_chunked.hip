@@ -304,8 +304,8 @@ template <int N, int T, int kWv, typename Tin, typename Tout, bool kTwoD, bool k
 __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
-    const float* __restrict__ dt_bias, Tout* __restrict__ y, int K, int Dc, int L, int H, int W,
-    int softplus, int n_groups, int n_wg) {
+    const float* __restrict__ dt_bias, Tout* __restrict__ y, const Tin* __restrict__ xt, int K,
+    int Dc, int L, int H, int W, int softplus, int n_groups, int n_wg) {
     static_assert(N % 4 == 0, "states go in pairs, and pairs alternate stage buffers");
     static_assert(kComputeWaves % kWv == 0, "whole channels per workgroup");
     constexpr int kPairs = N / 2;
@@ -399,9 +399,15 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         const int cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
         const int tl = cnt > 0 ? t0 : 0;  // keep addresses in range for empty runs
         load_run<T>(drow + tl, dv, cnt == T, cnt);
-        if constexpr (kTwoD)
-            load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
-        else
+        if constexpr (kTwoD) {
+            // directions 1 and 3 from the column-major copy when given: its
+            // rows are those directions' sequences, read like directions 0, 2
+            if ((k & 1) && xt)
+                load_run_2d<T>(xt + (static_cast<size_t>(b) * Dc + d) * L, k - 1, tl, H, W, L, uv,
+                               cnt);
+            else
+                load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
+        } else
             load_run<T>(urow + tl, uv, cnt == T, cnt);
     };
     const float* an = arow[g];
@@ -520,7 +526,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
 // Chunked full scan: picks the run length and waves per channel from L.
 namespace {
 template <int N, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh>
-vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y) {
+vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y, const void* xt) {
     constexpr int T = 13;  // positions per lane run
     constexpr int G = kComputeWaves / kWv;  // channels per workgroup
     const int n_groups = int((a.channels + G - 1) / G);
@@ -530,38 +536,41 @@ vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y) {
     hipLaunchKernelGGL((k_full_scan_chunked<N, T, kWv, Tin, Tout, kTwoD, kZoh>), grid, block, 0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,
-                       y, int(a.K), int(a.channels), int(a.L), int(a.H), int(a.W), a.softplus,
-                       n_groups, int(n_wg));
+                       y, static_cast<const Tin*>(xt), int(a.K), int(a.channels), int(a.L),
+                       int(a.H), int(a.W), a.softplus, n_groups, int(n_wg));
     return check_launch();
 }
 
 // Waves per channel from L: cover the sequence in one chunk where possible
 // (runs of 13 positions, 64 lanes per wave).
 template <int N, typename Tin, typename Tout, bool kTwoD, bool kZoh>
-vmb_status launch_chunked_waves(const ScanArgs& a, Tout* y) {
+vmb_status launch_chunked_waves(const ScanArgs& a, Tout* y, const void* xt) {
     const int64_t L = a.L;
-    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD, kZoh>(a, y);
-    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD, kZoh>(a, y);
-    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD, kZoh>(a, y);
+    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD, kZoh>(a, y, xt);
+    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD, kZoh>(a, y, xt);
+    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD, kZoh>(a, y, xt);
 }
 
 template <int N, typename Tin, typename Tout, bool kTwoD>
-vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y) {
-    return (a.options & VMB_SCAN_ZOH) ? launch_chunked_waves<N, Tin, Tout, kTwoD, true>(a, y)
-                                      : launch_chunked_waves<N, Tin, Tout, kTwoD, false>(a, y);
+vmb_status launch_chunked_impl(const ScanArgs& a, Tout* y, const void* xt) {
+    return (a.options & VMB_SCAN_ZOH) ? launch_chunked_waves<N, Tin, Tout, kTwoD, true>(a, y, xt)
+                                      : launch_chunked_waves<N, Tin, Tout, kTwoD, false>(a, y, xt);
 }
 }  // namespace
 
-vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq) {
+static_assert(4 * kWave * 13 == kChunkedOneChunkMaxL, "one pass of the four-wave form");
+
+vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq, const void* xt) {
     if (a.N != 16) return VMB_ERR_UNSUPPORTED;
     const bool two_d = a.layout == VMB_LAYOUT_2D;
     if (a.in_dt == VMB_F32)
-        return two_d ? launch_chunked_impl<16, float, float, true>(a, static_cast<float*>(y_seq))
-                     : launch_chunked_impl<16, float, float, false>(a, static_cast<float*>(y_seq));
-    if (two_d) return launch_chunked_impl<16, bf16_t, float, true>(a, static_cast<float*>(y_seq));
+        return two_d ? launch_chunked_impl<16, float, float, true>(a, static_cast<float*>(y_seq), xt)
+                     : launch_chunked_impl<16, float, float, false>(a, static_cast<float*>(y_seq),
+                                                                   nullptr);
+    if (two_d) return launch_chunked_impl<16, bf16_t, float, true>(a, static_cast<float*>(y_seq), xt);
     if (a.out_dt == VMB_BF16)
-        return launch_chunked_impl<16, bf16_t, bf16_t, false>(a, static_cast<bf16_t*>(y_seq));
-    return launch_chunked_impl<16, bf16_t, float, false>(a, static_cast<float*>(y_seq));
+        return launch_chunked_impl<16, bf16_t, bf16_t, false>(a, static_cast<bf16_t*>(y_seq), nullptr);
+    return launch_chunked_impl<16, bf16_t, float, false>(a, static_cast<float*>(y_seq), nullptr);
 }
 
 }  // namespace vmb

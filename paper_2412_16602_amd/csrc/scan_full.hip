@@ -126,13 +126,15 @@ vmb_status launch_full_scan(const ScanArgs& a) {
     if (tiles || use_chunked_full(a) || (!zoh && use_short_full(a))) {
         auto run = [&](void* y_seq, const void* xt) {
             if (tiles) return launch_full_tiles(a, y_seq, xt);
-            return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq);
+            return use_short_full(a) ? launch_full_short(a, y_seq) : launch_full_chunked(a, y_seq, xt);
         };
         if (a.layout == VMB_LAYOUT_SEQ) return run(a.y, nullptr);
-        // 2-D: the tile path reads directions 1 and 3 from column-major plane
+        // 2-D: the tile path, and the positions-over-lanes path on sequences of
+        // several chunks, read directions 1 and 3 from column-major plane
         // copies in the workspace
         const void* xt = nullptr;
-        if (tiles && full_ws_has_xt(a.batch, a.K, a.channels, a.L, a.N)) {
+        const bool chunked_long = !tiles && !use_short_full(a) && a.L > kChunkedOneChunkMaxL;
+        if ((tiles || chunked_long) && full_ws_has_xt(a.batch, a.K, a.channels, a.L, a.N)) {
             void* xtw = static_cast<char*>(a.ws) + full_ws_xt_offset(a.batch, a.K, a.channels, a.L);
             vmb_status st = launch_transpose_planes(a.u, xtw, a.batch, a.channels, a.H, a.W,
                                                     a.in_dt, a.stream);

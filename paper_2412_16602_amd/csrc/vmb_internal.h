@@ -196,7 +196,12 @@ vmb_status launch_channel_mean(const float* x, float* xm, int64_t batch, int64_t
                                int64_t L, hipStream_t s);
 // Positions-over-lanes full scan (N == 16); writes sequence-layout output to
 // y_seq (a.y for the sequence layout, the fp32 workspace for the 2-D one).
-vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq);
+// 2-D layout: xt, when given, holds the column-major copies of the input
+// planes, which directions 1 and 3 then read as contiguous rows.
+vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq, const void* xt);
+// Longest sequence that kernel covers in one pass (4 waves x 64 lanes x 13
+// positions); longer ones walk several chunks.
+constexpr int64_t kChunkedOneChunkMaxL = 3328;
 // Short sequences (L <= kShortMaxL, N == 16): whole sequences in segments of
 // 16 or 32 lanes of one wave; writes sequence-layout output to y_seq.
 constexpr int64_t kShortMaxL = 416;
@@ -215,13 +220,16 @@ bool tiles_take(const ScanArgs& a);
 // per-direction outputs), so directions 1 and 3 load contiguous rows.
 vmb_status launch_full_tiles(const ScanArgs& a, void* y_seq, const void* xt);
 // Full scan, 2-D layout: whether the workspace holds xt (the tile path's
-// shapes with planes the transpose kernel takes: L <= kMeanTransposeMaxL, so
-// H * (W + 1) <= 2 L; below 128 positions a plane spans a few cache lines and
-// the column-major reads gather it from L1 faster than a copy pass), where it
+// shapes with planes of 128 to 6144 positions: below, a plane spans a few
+// cache lines and the column-major reads gather it from L1 faster than a copy
+// pass; and the positions-over-lanes path's sequences of more than one
+// chunk, whose one-chunk form stages the plane in LDS instead), where it
 // starts (after the per-direction fp32 outputs), and its size (4 bytes per
 // element, either input type).
 inline bool full_ws_has_xt(int64_t batch, int64_t K, int64_t channels, int64_t L, int64_t N) {
-    return N == 16 && L >= 128 && L <= 6144 && batch * K * channels >= kTilesMinRows;
+    if (N != 16) return false;
+    const bool tiles = batch * K * channels >= kTilesMinRows;
+    return tiles ? (L >= 128 && L <= 6144) : L > kChunkedOneChunkMaxL;
 }
 inline size_t full_ws_xt_offset(int64_t batch, int64_t K, int64_t channels, int64_t L) {
     const size_t seq = static_cast<size_t>(batch) * K * channels * L;
