@@ -413,9 +413,6 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const float* an = arow[g];
     // One chunk, from this lane's delta / u run (dv, uv) to the stored y run.
     auto chunk_body = [&](int ci, float (&dv)[T], float (&uv)[T]) __attribute__((always_inline)) {
-        const int t0 = ci * chunk + run;
-        const int cnt = L - t0 < T ? (L - t0 > 0 ? L - t0 : 0) : T;
-        const bool full = cnt == T;
         float dl2[T], du[T], yv[T];
         float s2 = 0.0f;
         {
@@ -426,10 +423,14 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
 #pragma unroll
                 for (int i = 0; i < T; ++i) dv[i] += bias;
             }
+            // Positions past the end of the sequence (in the last chunk only)
+            // come after every valid position of it, in the lane's run, in
+            // lane order and in wave order: whatever they hold reaches no
+            // valid position's state and no stored output, so they need no
+            // masking.
 #pragma unroll
             for (int i = 0; i < T; ++i) {
-                // positions past the end act as the identity: a = 1, b = 0
-                const float dl = (full || i < cnt) ? dv[i] : 0.0f;
+                const float dl = dv[i];
                 dl2[i] = dl * kLog2e;
                 du[i] = dl * uv[i];
                 yv[i] = dskip * uv[i];
@@ -496,12 +497,12 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         }
         const int cnt = L - run < T ? (L - run > 0 ? L - run : 0) : T;
 #pragma unroll
-        for (int i = 0; i < T; ++i) dv0[i] = i < cnt ? to_f32(dsl[lane * T + i]) : 0.0f;
+        for (int i = 0; i < T; ++i) dv0[i] = to_f32(dsl[lane * T + i]);  // past the end: any
         if constexpr (kTwoD) {
             load_run_2d<T>(usl, k, cnt > 0 ? run : 0, H, W, L, uv0, cnt);
         } else {
 #pragma unroll
-            for (int i = 0; i < T; ++i) uv0[i] = i < cnt ? to_f32(usl[lane * T + i]) : 0.0f;
+            for (int i = 0; i < T; ++i) uv0[i] = to_f32(usl[lane * T + i]);
         }
     } else {
         load_chunk(0, dv0, uv0);
