@@ -21,11 +21,20 @@
 // (a1 a2, a2 b1 + b2), associative (Appendix A: the associative scan Mamba
 // runs in its kernel). Per (position, state): mul, exp2, mul, 3 fma.
 //
-// B and C rows are shared by every channel of a direction. The workgroup
-// copies each state's slice of them once, with coalesced loads, into a
-// triple-buffered LDS stage two states ahead of use; lanes then read their
-// runs from LDS (stride-13 words: conflict-free). One barrier per state
-// orders the stage and the cross-wave exchange.
+// States go in pairs, one workgroup barrier per pair: phase 1 (steps 1-2 up
+// to the wave's aggregate) before it, the cross-wave join and phase 2 after.
+// B and C rows are shared by every channel of a direction. Four copy waves
+// move each pair's slices of them once, straight from global memory into LDS
+// (global_load_lds), double-buffered: before barrier p they issue C of pair p
+// and B of pair p + 1. Lanes read their runs from LDS (stride-13 words:
+// conflict-free).
+//
+// Delta and u: a sequence of one chunk has each wave's ranges (2-D layout:
+// each channel's input plane, which every direction reads through its
+// cross-scan map) copied into LDS the same way before the first barrier and
+// the runs read from there; longer sequences load the runs from global
+// memory, the 2-D directions 1 and 3 from column-major plane copies when the
+// caller's workspace holds them.
 //
 // Workgroups are numbered so that the ones sharing a (batch, direction), and
 // therefore B and C, land on the same XCD and its L2.
