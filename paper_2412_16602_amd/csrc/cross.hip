@@ -329,6 +329,10 @@ bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
     return plane_fits(batch, channels, H, W);
 }
 
+bool cross_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
+    return plane_fits(batch, channels, H, W) || grid_fits(batch, channels, H, W);
+}
+
 vmb_status launch_transpose_planes(const void* x, void* xt, int64_t batch, int64_t channels,
                                    int64_t H, int64_t W, vmb_dtype dt, hipStream_t s) {
     if (plane_fits(batch, channels, H, W))

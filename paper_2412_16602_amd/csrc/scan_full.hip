@@ -138,12 +138,8 @@ vmb_status launch_full_scan(const ScanArgs& a) {
             void* xtw = static_cast<char*>(a.ws) + full_ws_xt_offset(a.batch, a.K, a.channels, a.L);
             vmb_status st = launch_transpose_planes(a.u, xtw, a.batch, a.channels, a.H, a.W,
                                                     a.in_dt, a.stream);
-            // maps too large for the transpose grid (nothing launched) keep
-            // the gathers through the cross-scan map
-            if (st == VMB_OK)
-                xt = xtw;
-            else if (st != VMB_ERR_UNSUPPORTED)
-                return st;
+            if (st != VMB_OK) return st;
+            xt = xtw;
         }
         vmb_status st = run(a.ws, xt);
         if (st != VMB_OK) return st;

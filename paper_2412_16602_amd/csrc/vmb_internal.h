@@ -173,6 +173,9 @@ vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t cha
 // Column-major copy of every (batch, channel) plane, xt[plane][w * H + h]
 // (direction 1's sequence); only for planes that cross_plane_fits accepts.
 bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W);
+// Whether the cross-scan / merge kernels take the map at all (a plane in LDS,
+// or 32 x 32 tiles within the grid limits); checked before any launch.
+bool cross_fits(int64_t batch, int64_t channels, int64_t H, int64_t W);
 vmb_status launch_transpose_planes(const void* x, void* xt, int64_t batch, int64_t channels,
                                    int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);
 // Merge with independent input / output element types (fp32 -> bf16 is used

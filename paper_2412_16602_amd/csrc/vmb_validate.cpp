@@ -178,6 +178,10 @@ vmb_status validate_scan(const ScanArgs& a, int mean_variant) {
         if (a.K != 4 || a.H < 1 || a.W < 1 || prod({a.H, a.W}) != a.L) return VMB_ERR_SHAPE;
     }
     if (!supported_n(a.N)) return VMB_ERR_UNSUPPORTED;
+    // the 2-D calls end with a merge pass: maps it cannot take fail here,
+    // before anything is launched
+    if (a.layout == VMB_LAYOUT_2D && !cross_fits(a.batch, a.channels, a.H, a.W))
+        return VMB_ERR_UNSUPPORTED;
     const unsigned known = VMB_MEAN_SKIP_PER_CHANNEL | VMB_MEAN_RAW | VMB_MEAN_NO_BROADCAST |
                            VMB_MEAN_POOLED | VMB_SCAN_ZOH | VMB_MEAN_TEST_GIVE_UP;
     if (a.options & ~known) return VMB_ERR_UNSUPPORTED;

@@ -32,7 +32,7 @@ VMB_SCAN_ZOH = 16
 STATUS = {0: "VMB_OK", 1: "VMB_ERR_NULL", 2: "VMB_ERR_SHAPE", 3: "VMB_ERR_DTYPE",
           4: "VMB_ERR_ALIGN", 5: "VMB_ERR_ALIAS", 6: "VMB_ERR_UNSUPPORTED",
           7: "VMB_ERR_WORKSPACE", 8: "VMB_ERR_HIP", 9: "VMB_ERR_INCOMPLETE"}
-VMB_OK, VMB_ERR_WORKSPACE, VMB_ERR_INCOMPLETE = 0, 7, 9
+VMB_OK, VMB_ERR_UNSUPPORTED, VMB_ERR_WORKSPACE, VMB_ERR_INCOMPLETE = 0, 6, 7, 9
 
 
 class VmbError(RuntimeError):

@@ -169,6 +169,13 @@ def test_workspace_rules(lib):
 
 
 def test_shape_limits(lib):
+    # 2-D maps beyond the merge pass's grid (65536 tiles of 32 columns) are
+    # refused before any launch; one tile fewer passes
+    for fn in ("vmb_selective_scan_fwd", "vmb_mean_scan_fwd"):
+        assert scan_call(lib, fn, layout=TWO_D, channels=1, N=16, H=1, W=1 << 21,
+                         L=1 << 21) == UNSUP
+        passes(lambda: scan_call(lib, fn, layout=TWO_D, channels=1, N=16, H=1,
+                                 W=(1 << 21) - 32, L=(1 << 21) - 32, ws_bytes=1 << 34))
     assert scan_call(lib, L=1 << 31) == SHAPE
     assert scan_call(lib, batch=1 << 20, channels=1 << 20) == SHAPE
     assert scan_call(lib, N=16, L=(1 << 31) // 8) == SHAPE

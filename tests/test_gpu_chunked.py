@@ -5,6 +5,7 @@ import pytest
 import torch
 
 import workloads
+from paper_2412_16602_amd import vmb
 from gpu_util import BF16_TOL, FP32_TOL, assert_close, log, oracle_seq, run_scan, to_f64
 from test_gpu_scan import merged_oracle
 
@@ -68,3 +69,23 @@ def test_softplus_off_and_no_bias():
     got = to_f64(run_scan(inp, "full", "seq", softplus=False, use_bias=False, delta=delta))
     ref = oracle_seq(inp, "full", "seq", softplus=False, use_bias=False, delta=delta)
     assert_close(got, ref, **FP32_TOL, what="softplus off")
+
+
+def test_2d_map_beyond_the_merge_grid_is_refused():
+    # a 1 x 2^21 map has 65536 tiles of 32 columns, more than the merge and
+    # transpose kernels' grid takes: the call returns VMB_ERR_UNSUPPORTED from
+    # its host checks and writes nothing
+    log("chunked full 2d 1x2097152 refused")
+    W = 1 << 21
+    f = torch.float32
+    x = torch.zeros(1, 1, 1, W, dtype=f, device="cuda")
+    delta = torch.zeros(1, 4, 1, W, dtype=f, device="cuda")
+    Bm = torch.zeros(1, 4, 16, W, dtype=f, device="cuda")
+    A = -torch.ones(4, 16, dtype=f, device="cuda")
+    y = torch.full((1, 1, 1, W), 7.0, dtype=f, device="cuda")
+    with pytest.raises(vmb.VmbError) as err:
+        vmb.vmb_selective_scan_fwd(x, delta, A, Bm, Bm, None, None, True, y,
+                                   layout=vmb.VMB_LAYOUT_2D)
+    assert err.value.status == vmb.VMB_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert bool((y == 7.0).all())
