@@ -132,9 +132,9 @@ vmb_status vmb_cross_merge(const void* ys, void* y, int64_t batch, int64_t chann
  *              bytes (may be NULL when that is 0); contents on entry are
  *              irrelevant and undefined on exit.
  * VMB_ERR_UNSUPPORTED also for 2D maps the merge pass cannot take: planes
- * beyond 48 KB whose rows or columns exceed 65535 tiles of 32 pixels, or
- * more than 2^24 (batch, channel) planes (the same rule holds for
- * vmb_mean_scan_fwd).
+ * larger than H * (W + 1) = 12288 fp32 words that need more than 65535 tiles
+ * of 32 pixels along a side, or that come in more than 2^24 (batch, channel)
+ * planes (the same rule holds for vmb_mean_scan_fwd).
  */
 vmb_status vmb_selective_scan_fwd(const void* u, const void* delta, const float* A,
                                   const void* B, const void* C, const float* D,
