@@ -34,7 +34,9 @@
 // cross-scan map) copied into LDS the same way before the first barrier and
 // the runs read from there; longer sequences load the runs from global
 // memory, the 2-D directions 1 and 3 from column-major plane copies when the
-// caller's workspace holds them.
+// caller's workspace holds them. The first chunk's timescales and
+// per-position products are formed before the first barrier: waves whose
+// data arrived early work while the others' loads are still in flight.
 //
 // Workgroups are numbered so that the ones sharing a (batch, direction), and
 // therefore B and C, land on the same XCD and its L2.
@@ -99,7 +101,10 @@ __device__ __forceinline__ void load_run(const bf16_t* p, float (&v)[T], bool fu
 // straight from the runs, each store instruction would touch every lane's
 // own cache lines; instead the wave passes the values through its own LDS
 // slice (stride T words: no bank conflicts) and stores them lane-contiguous,
-// 4 values per lane (aligned rows) or 1.
+// 4 values per lane (aligned rows) or 1. Whole fp32 quads go out as
+// non-temporal stores: nothing here reads them again, and streamed out they
+// do not sit dirty in L2 until the end of the kernel, which writes them back
+// after the last wave (the waves of a launch finish close together).
 template <int T, typename Tout>
 __device__ __forceinline__ void store_wave(Tout* dst, const float (&v)[T], float* slice, int lane,
                                            int nval, bool aligned4) {
@@ -114,7 +119,9 @@ __device__ __forceinline__ void store_wave(Tout* dst, const float (&v)[T], float
                 const float4 q = *reinterpret_cast<const float4*>(slice + 4 * j);
                 if (4 * j + 4 <= nval) {
                     if constexpr (sizeof(Tout) == 4) {
-                        *reinterpret_cast<float4*>(dst + 4 * j) = q;
+                        typedef float f32x4 __attribute__((ext_vector_type(4)));
+                        const f32x4 v = {q.x, q.y, q.z, q.w};
+                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(dst + 4 * j));
                     } else {
                         Tout o[4] = {from_f32<Tout>(q.x), from_f32<Tout>(q.y), from_f32<Tout>(q.z),
                                      from_f32<Tout>(q.w)};
@@ -163,14 +170,15 @@ __device__ __forceinline__ void load_run_2d(const Tin* plane, int k, int t0, int
 
 // Phase 1 of one state for one lane: a_i, b_i of its run (registers), the
 // run aggregate, the inclusive scan over the wave (Pin, Hin, kept for phase
-// 2), and this wave's aggregate published to xg[wv] by the last lane.
+// 2), and this wave's aggregate published by the last lane to xg[slot]
+// (slot kWv - 1 + w of the channel's row, see state_phase2).
 // With kZoh, Bbar u takes the zero-order-hold form (zoh_q, from the run's u
 // values uvr and inv_an = 1 / A_n) instead of Delta u.
 template <int T, typename Tin, bool kZoh = false>
 __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], const float (&du)[T],
                                              float s2, const Tin* bsrc, float (&a)[T],
                                              float (&bu)[T], float& Pin, float& Hin,
-                                             float (*xg)[2], int lane, int wv,
+                                             float (*xg)[2], int lane, int slot,
                                              const float (&uvr)[T], float inv_an) {
     float agg = 0.0f;
 #pragma unroll
@@ -185,8 +193,8 @@ __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], co
     Hin = agg;
     wave_scan(Pin, Hin);
     if (lane == kWave - 1) {
-        xg[wv][0] = Pin;
-        xg[wv][1] = Hin;
+        xg[slot][0] = Pin;
+        xg[slot][1] = Hin;
     }
 }
 
@@ -194,24 +202,37 @@ __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], co
 // channel's earlier waves and the previous chunk (*hcar, this wave's own copy
 // of the carry), the state entering this lane (lane - 1's inclusive scan
 // applied to it, read across lanes), then the re-walk of the run,
-// accumulating y_i += C_i h_i. Every wave of a channel composes the same
-// aggregates in the same order, so every copy of the carry into the next
-// chunk (the state leaving the channel's last wave) is the same.
-template <int T, int kWv, typename Tin>
+// accumulating y_i += C_i h_i.
+//
+// xg is the channel's row of 2 kWv - 1 slots: kWv - 1 identities (1, 0),
+// then the aggregates of waves 0 .. kWv - 1. In a chunk that carries nothing
+// out, wave w composes the kWv - 1 slots from w on (identities, then waves
+// 0 .. w - 1): the same count of steps for every wave, with no per-wave
+// selection. With kCarryOut (a later chunk follows) every wave composes all
+// kWv aggregates from the carry, which gives the state leaving the channel
+// (the same in every wave's copy), and takes cin from the chain on the way.
+template <int T, int kWv, bool kCarryOut, typename Tin>
 __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pin,
                                              float Hin, const Tin* csrc, float (&yv)[T],
-                                             const float (*xg)[2], float* hcar, int lane, int g,
-                                             int w) {
+                                             const float (*xg)[2], float* hcar, int lane, int w) {
     const float hc = *hcar;
     float cin = hc;
-    float cnext = hc;
+    if constexpr (kCarryOut) {
+        float cnext = hc;
 #pragma unroll
-    for (int j = 0; j < kWv; ++j) {
-        const float2 x = *reinterpret_cast<const float2*>(xg[g * kWv + j]);
-        cnext = __builtin_fmaf(x.x, cnext, x.y);
-        if (j + 1 < kWv && j + 1 == w) cin = cnext;
+        for (int j = 0; j < kWv; ++j) {
+            const float2 x = *reinterpret_cast<const float2*>(xg[kWv - 1 + j]);
+            cnext = __builtin_fmaf(x.x, cnext, x.y);
+            if (j + 1 < kWv && j + 1 == w) cin = cnext;
+        }
+        if (lane == 0) *hcar = cnext;
+    } else {
+#pragma unroll
+        for (int j = 0; j + 1 < kWv; ++j) {
+            const float2 x = *reinterpret_cast<const float2*>(xg[w + j]);
+            cin = __builtin_fmaf(x.x, cin, x.y);
+        }
     }
-    if (lane == 0) *hcar = cnext;
     // lane 0 starts from cin itself (the shift leaves its old value)
     float h = dpp<kWaveShr1, 0xf>(cin, __builtin_fmaf(Pin, cin, Hin));
 #pragma unroll
@@ -319,8 +340,10 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     static_assert(kComputeWaves % kWv == 0, "whole channels per workgroup");
     constexpr int kPairs = N / 2;
     constexpr int G = kComputeWaves / kWv;  // channels per workgroup
-    // per (parity, state of the pair, wave): aggregates exchanged across waves
-    __shared__ __align__(16) float xagg[2][2][kComputeWaves][2];
+    // per (parity, state of the pair, channel): aggregates exchanged across
+    // waves, after kWv - 1 identity slots (see state_phase2)
+    constexpr int kSlots = 2 * kWv - 1;
+    __shared__ __align__(16) float xagg[2][2][G][kSlots][2];
     __shared__ __align__(16) float arow[G][N];  // A rows of the workgroup's channels
     __shared__ float hcar[kComputeWaves][N];    // per wave: state carried into the next chunk
     // B and C slices of a pair of states, double-buffered (distinct arrays so
@@ -399,6 +422,15 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     if (w == 0)
         for (int n = lane; n < N; n += kWave) arow[g][n] = A[static_cast<size_t>(c) * N + n];
     for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
+    if constexpr (kWv > 1) {
+        // the identity slots of the channel's rows (both parities, both states)
+        constexpr int kId = kWv - 1;
+        if (w == 0 && lane < 4 * kId) {
+            const int par = lane / (2 * kId), st = (lane / kId) % 2;
+            xagg[par][st][g][lane % kId][0] = 1.0f;
+            xagg[par][st][g][lane % kId][1] = 0.0f;
+        }
+    }
     const int run = (w * kWave + lane) * T;  // this lane's first position inside a chunk
 
     // This lane's run of delta and u for chunk ci; chunk 0's loads are issued
@@ -421,9 +453,12 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     };
     const float* an = arow[g];
     // One chunk, from this lane's delta / u run (dv, uv) to the stored y run.
-    auto chunk_body = [&](int ci, float (&dv)[T], float (&uv)[T]) __attribute__((always_inline)) {
-        float dl2[T], du[T], yv[T];
-        float s2 = 0.0f;
+    // Per position of the lane's run: the timescale (delta through softplus),
+    // its log2(e) multiple dl2, the products du = delta u and D u (yv, where
+    // the outputs accumulate), and the run's sum of dl2.
+    auto prep = [&](float (&dv)[T], const float (&uv)[T], float (&dl2)[T], float (&du)[T],
+                    float (&yv)[T], float& s2) __attribute__((always_inline)) {
+        s2 = 0.0f;
         {
             if (sp) {
 #pragma unroll
@@ -446,30 +481,43 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
                 s2 += dl2[i];
             }
         }
+    };
+    // The state steps of chunk ci and the store of its outputs.
+    auto chunk_steps = [&](int ci, const float (&dl2)[T], const float (&du)[T], float (&yv)[T],
+                           float s2, const float (&uv)[T]) __attribute__((always_inline)) {
         // One pair step per barrier: phase 1 reads B of the pair (published
         // by the previous barrier), the barrier publishes the wave aggregates
         // and C of the pair, phase 2 reads them.
         auto pair_step = [&](int n0, Tin (*bcur)[kStageMax], Tin (*ccur)[kStageMax],
-                             float (*xq)[kComputeWaves][2]) {
+                             float (*xq)[G][kSlots][2], auto carry_out) {
+            constexpr bool kOut = decltype(carry_out)::value;
             const float2 a01 = *reinterpret_cast<const float2*>(an + n0);
             const float inv0 = kZoh ? 1.0f / a01.x : 0.0f, inv1 = kZoh ? 1.0f / a01.y : 0.0f;
             float a0[T], bu0[T], a1[T], bu1[T];
             float Pin0, Hin0, Pin1, Hin1;
             state_phase1<T, Tin, kZoh>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pin0, Hin0,
-                                       xq[0], lane, wv, uv, inv0);
+                                       xq[0][g], lane, kWv - 1 + w, uv, inv0);
             state_phase1<T, Tin, kZoh>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pin1, Hin1,
-                                       xq[1], lane, wv, uv, inv1);
+                                       xq[1][g], lane, kWv - 1 + w, uv, inv1);
             __syncthreads();
-            state_phase2<T, kWv>(a0, bu0, Pin0, Hin0, &ccur[0][run], yv, xq[0], &hcar[wv][n0], lane,
-                                 g, w);
-            state_phase2<T, kWv>(a1, bu1, Pin1, Hin1, &ccur[1][run], yv, xq[1], &hcar[wv][n0 + 1],
-                                 lane, g, w);
+            state_phase2<T, kWv, kOut>(a0, bu0, Pin0, Hin0, &ccur[0][run], yv, xq[0][g],
+                                       &hcar[wv][n0], lane, w);
+            state_phase2<T, kWv, kOut>(a1, bu1, Pin1, Hin1, &ccur[1][run], yv, xq[1][g],
+                                       &hcar[wv][n0 + 1], lane, w);
         };
+        // the last chunk carries nothing out (separate loops: the choice is
+        // made once per chunk)
+        auto pairs = [&](auto carry_out) {
 #pragma unroll 1
-        for (int q = 0; q < kPairs; q += 2) {
-            pair_step(2 * q, bst0, cst0, xagg[0]);
-            pair_step(2 * q + 2, bst1, cst1, xagg[1]);
-        }
+            for (int q = 0; q < kPairs; q += 2) {
+                pair_step(2 * q, bst0, cst0, xagg[0], carry_out);
+                pair_step(2 * q + 2, bst1, cst1, xagg[1], carry_out);
+            }
+        };
+        if (ci + 1 < nchunks)
+            pairs(std::true_type{});
+        else
+            pairs(std::false_type{});
         const int seg0 = ci * chunk + w * kWave * T;  // this wave's first position
         if (d_ok && seg0 < L)
             store_wave<T>(yrow + seg0, yv, ystage[wv], lane, min(kWave * T, L - seg0),
@@ -517,17 +565,17 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         load_chunk(0, dv0, uv0);
     }
 
+    // the first chunk's per-position products before the first barrier: waves
+    // whose loads arrived early work while the others' are still in flight
+    float dl2[T], du[T], yv[T], s2;
+    prep(dv0, uv0, dl2, du, yv, s2);
     __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
-    // keep every use of the loaded values after the barrier (the compiler
-    // would otherwise wait for the loads before it)
-#pragma unroll
-    for (int i = 0; i < T; ++i) asm volatile("" : "+v"(dv0[i]), "+v"(uv0[i]));
-
-    chunk_body(0, dv0, uv0);
+    chunk_steps(0, dl2, du, yv, s2, uv0);
     for (int ci = 1; ci < nchunks; ++ci) {
         float dv[T], uv[T];
         load_chunk(ci, dv, uv);
-        chunk_body(ci, dv, uv);
+        prep(dv, uv, dl2, du, yv, s2);
+        chunk_steps(ci, dl2, du, yv, s2, uv);
     }
 }
 
