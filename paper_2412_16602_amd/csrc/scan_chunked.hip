@@ -33,10 +33,12 @@
 // each channel's input plane, which every direction reads through its
 // cross-scan map) copied into LDS the same way before the first barrier and
 // the runs read from there; longer sequences load the runs from global
-// memory, the 2-D directions 1 and 3 from column-major plane copies when the
-// caller's workspace holds them. The first chunk's timescales and
-// per-position products are formed before the first barrier: waves whose
-// data arrived early work while the others' loads are still in flight.
+// memory (whole runs of rows with vector loads), the 2-D directions 1 and 3
+// from column-major plane copies when the caller's workspace holds them.
+// Sequences of one chunk have a kernel of their own (kOne), which carries
+// no state out of the chunk and forms its timescales and per-position
+// products before the first barrier: waves whose data arrived early work
+// while the others' loads are still in flight.
 //
 // Workgroups are numbered so that the ones sharing a (batch, direction), and
 // therefore B and C, land on the same XCD and its L2.
@@ -168,10 +170,30 @@ __device__ __forceinline__ void load_run_2d(const Tin* plane, int k, int t0, int
     }
 }
 
+// load_run_2d from global memory: a whole run of a row-major direction
+// (k = 0, or k = 2 reversed) is T consecutive elements of the plane, read
+// with vector loads as in the sequence layout; other runs element by element.
+template <int T, typename Tin>
+__device__ __forceinline__ void load_run_2d_global(const Tin* plane, int k, int t0, int H, int W,
+                                                   int L, float (&v)[T], int cnt) {
+    if ((k & 1) == 0 && cnt == T) {
+        if (k == 0) {
+            load_run<T>(plane + t0, v, true, T);
+        } else {
+            float w[T];
+            load_run<T>(plane + (L - t0 - T), w, true, T);
+#pragma unroll
+            for (int i = 0; i < T; ++i) v[i] = w[T - 1 - i];
+        }
+        return;
+    }
+    load_run_2d<T>(plane, k, t0, H, W, L, v, cnt);
+}
+
 // Phase 1 of one state for one lane: a_i, b_i of its run (registers), the
 // run aggregate, the inclusive scan over the wave (Pin, Hin, kept for phase
 // 2), and this wave's aggregate published by the last lane to xg[slot]
-// (slot kWv - 1 + w of the channel's row, see state_phase2).
+// (the channel's row, see state_phase2).
 // With kZoh, Bbar u takes the zero-order-hold form (zoh_q, from the run's u
 // values uvr and inv_an = 1 / A_n) instead of Delta u.
 template <int T, typename Tin, bool kZoh = false>
@@ -204,13 +226,13 @@ __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], co
 // applied to it, read across lanes), then the re-walk of the run,
 // accumulating y_i += C_i h_i.
 //
-// xg is the channel's row of 2 kWv - 1 slots: kWv - 1 identities (1, 0),
-// then the aggregates of waves 0 .. kWv - 1. In a chunk that carries nothing
-// out, wave w composes the kWv - 1 slots from w on (identities, then waves
-// 0 .. w - 1): the same count of steps for every wave, with no per-wave
-// selection. With kCarryOut (a later chunk follows) every wave composes all
-// kWv aggregates from the carry, which gives the state leaving the channel
-// (the same in every wave's copy), and takes cin from the chain on the way.
+// xg is the channel's row of slots. With kCarryOut (chunks pass a carry on)
+// it holds the aggregates of waves 0 .. kWv - 1; every wave composes all of
+// them from the carry, which gives the state leaving the channel (the same
+// in every wave's copy), and takes cin from the chain on the way. Without,
+// the row starts with kWv - 1 identities (1, 0) and wave w composes the
+// kWv - 1 slots from w on (identities, then waves 0 .. w - 1): the same
+// count of steps for every wave, with no per-wave selection.
 template <int T, int kWv, bool kCarryOut, typename Tin>
 __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pin,
                                              float Hin, const Tin* csrc, float (&yv)[T],
@@ -221,7 +243,7 @@ __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&
         float cnext = hc;
 #pragma unroll
         for (int j = 0; j < kWv; ++j) {
-            const float2 x = *reinterpret_cast<const float2*>(xg[kWv - 1 + j]);
+            const float2 x = *reinterpret_cast<const float2*>(xg[j]);
             cnext = __builtin_fmaf(x.x, cnext, x.y);
             if (j + 1 < kWv && j + 1 == w) cin = cnext;
         }
@@ -330,7 +352,10 @@ __device__ __forceinline__ void stage_one(const Tin* base, int p, int s, Tin* ds
 // LDS copies above) are done: vmcnt(0), other counters untouched.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
-template <int N, int T, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh>
+// kOne: the sequence fits one chunk (the launcher's choice), which then
+// carries no state out; otherwise every chunk passes its carry on (the last
+// one's is formed and not read).
+template <int N, int T, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh, bool kOne>
 __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
@@ -341,8 +366,9 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     constexpr int kPairs = N / 2;
     constexpr int G = kComputeWaves / kWv;  // channels per workgroup
     // per (parity, state of the pair, channel): aggregates exchanged across
-    // waves, after kWv - 1 identity slots (see state_phase2)
-    constexpr int kSlots = 2 * kWv - 1;
+    // waves, after kLead identity slots (see state_phase2)
+    constexpr int kLead = kOne ? kWv - 1 : 0;  // identity slots before the waves'
+    constexpr int kSlots = kLead + kWv;
     __shared__ __align__(16) float xagg[2][2][G][kSlots][2];
     __shared__ __align__(16) float arow[G][N];  // A rows of the workgroup's channels
     __shared__ float hcar[kComputeWaves][N];    // per wave: state carried into the next chunk
@@ -367,7 +393,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     const int lane = tid % kWave;
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
     constexpr int chunk = kWv * kWave * T;
-    const int nchunks = (L + chunk - 1) / chunk;
+    const int nchunks = kOne ? 1 : (L + chunk - 1) / chunk;
     const bool vec4 = (L % (16 / static_cast<int>(sizeof(Tin)))) == 0;
     // A sequence that fits one chunk, in rows of whole 16-byte pieces, has its
     // delta and u runs copied into LDS with coalesced pieces before the first
@@ -422,9 +448,9 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     if (w == 0)
         for (int n = lane; n < N; n += kWave) arow[g][n] = A[static_cast<size_t>(c) * N + n];
     for (int n = lane; n < N; n += kWave) hcar[wv][n] = 0.0f;
-    if constexpr (kWv > 1) {
+    if constexpr (kLead > 0) {
         // the identity slots of the channel's rows (both parities, both states)
-        constexpr int kId = kWv - 1;
+        constexpr int kId = kLead;
         if (w == 0 && lane < 4 * kId) {
             const int par = lane / (2 * kId), st = (lane / kId) % 2;
             xagg[par][st][g][lane % kId][0] = 1.0f;
@@ -444,10 +470,10 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
             // directions 1 and 3 from the column-major copy when given: its
             // rows are those directions' sequences, read like directions 0, 2
             if ((k & 1) && xt)
-                load_run_2d<T>(xt + (static_cast<size_t>(b) * Dc + d) * L, k - 1, tl, H, W, L, uv,
-                               cnt);
+                load_run_2d_global<T>(xt + (static_cast<size_t>(b) * Dc + d) * L, k - 1, tl, H, W,
+                                      L, uv, cnt);
             else
-                load_run_2d<T>(urow, k, tl, H, W, L, uv, cnt);
+                load_run_2d_global<T>(urow, k, tl, H, W, L, uv, cnt);
         } else
             load_run<T>(urow + tl, uv, cnt == T, cnt);
     };
@@ -489,35 +515,27 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         // by the previous barrier), the barrier publishes the wave aggregates
         // and C of the pair, phase 2 reads them.
         auto pair_step = [&](int n0, Tin (*bcur)[kStageMax], Tin (*ccur)[kStageMax],
-                             float (*xq)[G][kSlots][2], auto carry_out) {
-            constexpr bool kOut = decltype(carry_out)::value;
+                             float (*xq)[G][kSlots][2]) {
+            constexpr bool kOut = !kOne;  // chunks pass a carry on
             const float2 a01 = *reinterpret_cast<const float2*>(an + n0);
             const float inv0 = kZoh ? 1.0f / a01.x : 0.0f, inv1 = kZoh ? 1.0f / a01.y : 0.0f;
             float a0[T], bu0[T], a1[T], bu1[T];
             float Pin0, Hin0, Pin1, Hin1;
             state_phase1<T, Tin, kZoh>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pin0, Hin0,
-                                       xq[0][g], lane, kWv - 1 + w, uv, inv0);
+                                       xq[0][g], lane, kLead + w, uv, inv0);
             state_phase1<T, Tin, kZoh>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pin1, Hin1,
-                                       xq[1][g], lane, kWv - 1 + w, uv, inv1);
+                                       xq[1][g], lane, kLead + w, uv, inv1);
             __syncthreads();
             state_phase2<T, kWv, kOut>(a0, bu0, Pin0, Hin0, &ccur[0][run], yv, xq[0][g],
                                        &hcar[wv][n0], lane, w);
             state_phase2<T, kWv, kOut>(a1, bu1, Pin1, Hin1, &ccur[1][run], yv, xq[1][g],
                                        &hcar[wv][n0 + 1], lane, w);
         };
-        // the last chunk carries nothing out (separate loops: the choice is
-        // made once per chunk)
-        auto pairs = [&](auto carry_out) {
 #pragma unroll 1
-            for (int q = 0; q < kPairs; q += 2) {
-                pair_step(2 * q, bst0, cst0, xagg[0], carry_out);
-                pair_step(2 * q + 2, bst1, cst1, xagg[1], carry_out);
-            }
-        };
-        if (ci + 1 < nchunks)
-            pairs(std::true_type{});
-        else
-            pairs(std::false_type{});
+        for (int q = 0; q < kPairs; q += 2) {
+            pair_step(2 * q, bst0, cst0, xagg[0]);
+            pair_step(2 * q + 2, bst1, cst1, xagg[1]);
+        }
         const int seg0 = ci * chunk + w * kWave * T;  // this wave's first position
         if (d_ok && seg0 < L)
             store_wave<T>(yrow + seg0, yv, ystage[wv], lane, min(kWave * T, L - seg0),
@@ -565,17 +583,28 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
         load_chunk(0, dv0, uv0);
     }
 
-    // the first chunk's per-position products before the first barrier: waves
-    // whose loads arrived early work while the others' are still in flight
     float dl2[T], du[T], yv[T], s2;
-    prep(dv0, uv0, dl2, du, yv, s2);
-    __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
+    if constexpr (kOne) {
+        // the per-position products before the first barrier: waves whose
+        // loads arrived early work while the others' are still in flight
+        prep(dv0, uv0, dl2, du, yv, s2);
+        __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
+    } else {
+        __syncthreads();  // pairs with the copy waves' first barrier (B of pair 0)
+        // keep every use of the loaded values after the barrier (the compiler
+        // would otherwise wait for the loads before it)
+#pragma unroll
+        for (int i = 0; i < T; ++i) asm volatile("" : "+v"(dv0[i]), "+v"(uv0[i]));
+        prep(dv0, uv0, dl2, du, yv, s2);
+    }
     chunk_steps(0, dl2, du, yv, s2, uv0);
-    for (int ci = 1; ci < nchunks; ++ci) {
-        float dv[T], uv[T];
-        load_chunk(ci, dv, uv);
-        prep(dv, uv, dl2, du, yv, s2);
-        chunk_steps(ci, dl2, du, yv, s2, uv);
+    if constexpr (!kOne) {
+        for (int ci = 1; ci < nchunks; ++ci) {
+            float dv[T], uv[T];
+            load_chunk(ci, dv, uv);
+            prep(dv, uv, dl2, du, yv, s2);
+            chunk_steps(ci, dl2, du, yv, s2, uv);
+        }
     }
 }
 
@@ -583,7 +612,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
 
 // Chunked full scan: picks the run length and waves per channel from L.
 namespace {
-template <int N, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh>
+template <int N, int kWv, typename Tin, typename Tout, bool kTwoD, bool kZoh, bool kOne>
 vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y, const void* xt) {
     constexpr int T = 13;  // positions per lane run
     constexpr int G = kComputeWaves / kWv;  // channels per workgroup
@@ -591,7 +620,8 @@ vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y, const void* xt) {
     const long long n_wg = static_cast<long long>(n_groups) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
     const dim3 grid(static_cast<unsigned>(n_wg)), block(kStageThreads);
-    hipLaunchKernelGGL((k_full_scan_chunked<N, T, kWv, Tin, Tout, kTwoD, kZoh>), grid, block, 0, a.stream,
+    hipLaunchKernelGGL((k_full_scan_chunked<N, T, kWv, Tin, Tout, kTwoD, kZoh, kOne>), grid, block,
+                       0, a.stream,
                        static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
                        static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D, a.dt_bias,
                        y, static_cast<const Tin*>(xt), int(a.K), int(a.channels), int(a.L),
@@ -600,13 +630,16 @@ vmb_status launch_chunked_wv(const ScanArgs& a, Tout* y, const void* xt) {
 }
 
 // Waves per channel from L: cover the sequence in one chunk where possible
-// (runs of 13 positions, 64 lanes per wave).
+// (runs of 13 positions, 64 lanes per wave); longer sequences take chunks of
+// the four-wave form.
 template <int N, typename Tin, typename Tout, bool kTwoD, bool kZoh>
 vmb_status launch_chunked_waves(const ScanArgs& a, Tout* y, const void* xt) {
     const int64_t L = a.L;
-    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD, kZoh>(a, y, xt);
-    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD, kZoh>(a, y, xt);
-    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD, kZoh>(a, y, xt);
+    if (L > kChunkedOneChunkMaxL)
+        return launch_chunked_wv<N, 4, Tin, Tout, kTwoD, kZoh, false>(a, y, xt);
+    if (L > 2 * kWave * 13) return launch_chunked_wv<N, 4, Tin, Tout, kTwoD, kZoh, true>(a, y, xt);
+    if (L > kWave * 13) return launch_chunked_wv<N, 2, Tin, Tout, kTwoD, kZoh, true>(a, y, xt);
+    return launch_chunked_wv<N, 1, Tin, Tout, kTwoD, kZoh, true>(a, y, xt);
 }
 
 template <int N, typename Tin, typename Tout, bool kTwoD>
