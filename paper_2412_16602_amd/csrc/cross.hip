@@ -125,9 +125,9 @@ __device__ __forceinline__ Vec<T, V> load_vec(const T* p) {
     return r;
 }
 
-template <typename T, int V>
+template <typename T, int V, bool kNt = false>
 __device__ __forceinline__ void store_vec(T* p, const Vec<T, V>& r) {
-    __builtin_memcpy(__builtin_assume_aligned(p, sizeof(r)), &r, sizeof(r));
+    store_out<kNt>(reinterpret_cast<Vec<T, V>*>(p), r);
 }
 
 // V elements per lane; L % V == 0 and 16-byte aligned planes when V > 1.
@@ -135,7 +135,7 @@ __device__ __forceinline__ void store_vec(T* p, const Vec<T, V>& r) {
 // sequence), to xs[plane][L].
 // TPP threads per plane, kPlaneThreads / TPP planes per workgroup, each with
 // its share of the LDS (small planes are batched, one wave each).
-template <typename T, int V, bool kAll, int TPP>
+template <typename T, int V, bool kAll, int TPP, bool kNt>
 __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __restrict__ x,
                                                                     T* __restrict__ xs, int Dc,
                                                                     int H, int W, int nplanes) {
@@ -171,11 +171,11 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
         if (!active || j >= nv) break;
         const int p = j * V;
         if constexpr (kAll) {
-            store_vec<T, V>(out0 + p, v[i]);
+            store_vec<T, V, kNt>(out0 + p, v[i]);
             Vec<T, V> r;
 #pragma unroll
             for (int e = 0; e < V; ++e) r.v[e] = v[i].v[V - 1 - e];
-            store_vec<T, V>(out2 + (L - V - p), r);
+            store_vec<T, V, kNt>(out2 + (L - V - p), r);
         }
 #pragma unroll
         for (int e = 0; e < V; ++e) {
@@ -194,12 +194,12 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_scan_plane(const T* __r
             v.v[e] = tile[h * Wp + w];
             r.v[V - 1 - e] = v.v[e];
         }
-        store_vec<T, V>(out1 + q, v);
-        if constexpr (kAll) store_vec<T, V>(out3 + (L - V - q), r);
+        store_vec<T, V, kNt>(out1 + q, v);
+        if constexpr (kAll) store_vec<T, V, kNt>(out3 + (L - V - q), r);
     }
 }
 
-template <typename Tin, typename Tout, int V, int TPP>
+template <typename Tin, typename Tout, int V, int TPP, bool kNt>
 __global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* __restrict__ ys,
                                                                      Tout* __restrict__ y, int Dc,
                                                                      int H, int W, int nplanes) {
@@ -259,7 +259,7 @@ __global__ __launch_bounds__(kPlaneThreads) void k_cross_merge_plane(const Tin* 
             const float s02 = to_f32(a0[i].v[e]) + to_f32(a2[i].v[V - 1 - e]);
             o.v[e] = from_f32<Tout>(s02 + s13[h * Wp + w]);
         }
-        store_vec<Tout, V>(dst + p, o);
+        store_vec<Tout, V, kNt>(dst + p, o);
     }
 }
 
@@ -293,11 +293,21 @@ void launch_scan_tpp(const T* xi, T* xo, int64_t planes, int c, int h, int w, hi
     const int ppw = kPlaneThreads / tpp;
     const dim3 grid(static_cast<unsigned>((planes + ppw - 1) / ppw)), block(kPlaneThreads);
     const int np = static_cast<int>(planes);
-    if (tpp == 64)
-        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 64>), grid, block, 0, s, xi, xo, c, h, w, np);
+    // non-temporal stores for planes of whole cache lines (V > 1 only: others
+    // are not)
+    const bool nt = V > 1 && whole_lines(int64_t(h) * w, sizeof(T));
+    if (tpp == 64 && nt)
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 64, V != 1>), grid, block, 0, s, xi, xo, c,
+                           h, w, np);
+    else if (tpp == 64)
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 64, false>), grid, block, 0, s, xi, xo, c,
+                           h, w, np);
+    else if (nt)
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, kPlaneThreads, V != 1>), grid, block, 0, s,
+                           xi, xo, c, h, w, np);
     else
-        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, kPlaneThreads>), grid, block, 0, s, xi, xo,
-                           c, h, w, np);
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, kPlaneThreads, false>), grid, block, 0, s,
+                           xi, xo, c, h, w, np);
 }
 
 template <bool kAll>
@@ -373,11 +383,19 @@ void launch_merge_tpp(const Tin* in, Tout* out, int64_t planes, int c, int h, in
     const int ppw = kPlaneThreads / tpp;
     const dim3 grid(static_cast<unsigned>((planes + ppw - 1) / ppw)), block(kPlaneThreads);
     const int np = static_cast<int>(planes);
-    if (tpp == 64)
-        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, 64>), grid, block, 0, s, in, out, c, h, w, np);
-    else
-        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, kPlaneThreads>), grid, block, 0, s, in, out,
+    const bool nt = V > 1 && whole_lines(int64_t(h) * w, sizeof(Tout));
+    if (tpp == 64 && nt)
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, 64, V != 1>), grid, block, 0, s, in, out,
                            c, h, w, np);
+    else if (tpp == 64)
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, 64, false>), grid, block, 0, s, in, out,
+                           c, h, w, np);
+    else if (nt)
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, kPlaneThreads, V != 1>), grid, block, 0,
+                           s, in, out, c, h, w, np);
+    else
+        hipLaunchKernelGGL((k_cross_merge_plane<Tin, Tout, V, kPlaneThreads, false>), grid, block, 0,
+                           s, in, out, c, h, w, np);
 }
 
 namespace {

@@ -67,20 +67,31 @@ __device__ __forceinline__ void load4(const bf16_t* p, float (&v)[4], bool vec, 
     }
 }
 
+template <bool kNt>
 __device__ __forceinline__ void store4(float* p, const float (&v)[4], bool vec, int cnt) {
     if (vec) {
-        *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+        if constexpr (kNt)
+            store_out<true>(reinterpret_cast<float4*>(p), make_float4(v[0], v[1], v[2], v[3]));
+        else
+            *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
     } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             if (e < cnt) p[e] = v[e];
     }
 }
+template <bool kNt>
 __device__ __forceinline__ void store4(bf16_t* p, const float (&v)[4], bool vec, int cnt) {
     if (vec) {
         bf16_t o[4] = {from_f32<bf16_t>(v[0]), from_f32<bf16_t>(v[1]), from_f32<bf16_t>(v[2]),
                        from_f32<bf16_t>(v[3])};
-        __builtin_memcpy(p, o, sizeof(o));
+        if constexpr (kNt) {
+            unsigned long long q;
+            __builtin_memcpy(&q, o, sizeof(o));
+            store_out<true>(reinterpret_cast<unsigned long long*>(p), q);
+        } else {
+            __builtin_memcpy(p, o, sizeof(o));
+        }
     } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -105,7 +116,7 @@ __device__ __forceinline__ void row8(const bf16_t* r, int off, float (&v)[8]) {
     }
 }
 
-template <typename Tin, typename Tout, bool kTwoD, bool kZoh>
+template <typename Tin, typename Tout, bool kTwoD, bool kZoh, bool kNt>
 __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
@@ -275,11 +286,12 @@ __global__ __launch_bounds__(kTileThreads) void k_full_scan_tiles(
             }
             if (ld_ok) {
                 if (t >= tnew) {
-                    store4(yrow + t, o, in_aligned, 4);
+                    store4<kNt>(yrow + t, o, in_aligned, 4);
                 } else {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        if (t + e >= tnew) store4(yrow + t + e, {o[e], 0.0f, 0.0f, 0.0f}, false, 1);
+                        if (t + e >= tnew)
+                            store4<false>(yrow + t + e, {o[e], 0.0f, 0.0f, 0.0f}, false, 1);
                 }
             }
         }
@@ -291,12 +303,21 @@ vmb_status launch_tiles_zoh(const ScanArgs& a, Tout* y, const void* xt) {
     const int n_cg = int((a.channels + kWave - 1) / kWave);
     const long long n_wg = static_cast<long long>(n_cg) * a.K * a.batch;
     if (n_wg > 0x7fffffffLL) return VMB_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL((k_full_scan_tiles<Tin, Tout, kTwoD, kZoh>), dim3(static_cast<unsigned>(n_wg)),
-                       dim3(kTileThreads), 0, a.stream, static_cast<const Tin*>(a.u),
-                       static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
-                       static_cast<const Tin*>(a.C), a.D, a.dt_bias, y, static_cast<const Tin*>(xt),
-                       int(a.K), int(a.channels),
-                       int(a.L), int(a.H), int(a.W), a.softplus, n_cg, int(n_wg));
+    // non-temporal output stores for rows of whole cache lines
+    if (whole_lines(a.L, sizeof(Tout)))
+        hipLaunchKernelGGL((k_full_scan_tiles<Tin, Tout, kTwoD, kZoh, true>),
+                           dim3(static_cast<unsigned>(n_wg)), dim3(kTileThreads), 0, a.stream,
+                           static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
+                           static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D,
+                           a.dt_bias, y, static_cast<const Tin*>(xt), int(a.K), int(a.channels),
+                           int(a.L), int(a.H), int(a.W), a.softplus, n_cg, int(n_wg));
+    else
+        hipLaunchKernelGGL((k_full_scan_tiles<Tin, Tout, kTwoD, kZoh, false>),
+                           dim3(static_cast<unsigned>(n_wg)), dim3(kTileThreads), 0, a.stream,
+                           static_cast<const Tin*>(a.u), static_cast<const Tin*>(a.delta), a.A,
+                           static_cast<const Tin*>(a.B), static_cast<const Tin*>(a.C), a.D,
+                           a.dt_bias, y, static_cast<const Tin*>(xt), int(a.K), int(a.channels),
+                           int(a.L), int(a.H), int(a.W), a.softplus, n_cg, int(n_wg));
     return check_launch();
 }
 

@@ -32,6 +32,39 @@ __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
     return r;
 }
 
+// Store of one value of 2, 4, 8 or 16 bytes at p (aligned to its size),
+// non-temporal with kNt: outputs nothing in the kernel reads again then
+// stream out instead of sitting dirty in L2 until the kernel ends. Launchers
+// choose kNt only for rows of whole 128-byte lines (whole_lines): stores that
+// cover parts of lines, streamed out one by one, cost more than merging them
+// in L2.
+template <bool kNt, typename T>
+__device__ __forceinline__ void store_out(T* p, const T& v) {
+    constexpr int kBytes = static_cast<int>(sizeof(T));
+    if constexpr (!kNt) {
+        __builtin_memcpy(__builtin_assume_aligned(p, kBytes), &v, kBytes);
+    } else if constexpr (kBytes == 16) {
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        u32x4 x;
+        __builtin_memcpy(&x, &v, 16);
+        __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(p));
+    } else if constexpr (kBytes == 8) {
+        typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+        u32x2 x;
+        __builtin_memcpy(&x, &v, 8);
+        __builtin_nontemporal_store(x, reinterpret_cast<u32x2*>(p));
+    } else if constexpr (kBytes == 4) {
+        unsigned int x;
+        __builtin_memcpy(&x, &v, 4);
+        __builtin_nontemporal_store(x, reinterpret_cast<unsigned int*>(p));
+    } else {
+        static_assert(kBytes == 2, "2, 4, 8 or 16 bytes");
+        unsigned short x;
+        __builtin_memcpy(&x, &v, 2);
+        __builtin_nontemporal_store(x, reinterpret_cast<unsigned short*>(p));
+    }
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 

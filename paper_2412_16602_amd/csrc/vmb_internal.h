@@ -205,6 +205,10 @@ vmb_status launch_full_chunked(const ScanArgs& a, void* y_seq, const void* xt);
 // Longest sequence that kernel covers in one pass (4 waves x 64 lanes x 13
 // positions); longer ones walk several chunks.
 constexpr int64_t kChunkedOneChunkMaxL = 3328;
+
+// Rows of L elements of size bytes are whole 128-byte cache lines (kernels
+// store such rows non-temporally).
+inline bool whole_lines(int64_t L, int size) { return (L * size) % 128 == 0; }
 // Short sequences (L <= kShortMaxL, N == 16): whole sequences in segments of
 // 16 or 32 lanes of one wave; writes sequence-layout output to y_seq.
 constexpr int64_t kShortMaxL = 416;
