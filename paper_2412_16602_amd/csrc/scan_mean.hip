@@ -73,26 +73,27 @@ struct StoreOpts {
 
 // Store ytilde at position t for the channels d0 + wv, d0 + wv + step, ...
 // below d1 of sequence bk (sequence layout).
-template <typename Tin, typename Tout>
+template <typename Tin, typename Tout, bool kNt = false>
 __device__ __forceinline__ void store_reduced(float yt, Tout* __restrict__ y,
                                               const Tin* __restrict__ u,
                                               const float* __restrict__ D, StoreOpts so,
                                               size_t bk, int k, int Dc, int L, int t, int wv,
                                               int step, int d0, int d1) {
     if (so.no_bcast) {
-        if (wv == 0 && d0 == 0) y[bk * L + t] = from_f32<Tout>(yt);
+        if (wv == 0 && d0 == 0) store_out<kNt>(y + bk * L + t, from_f32<Tout>(yt));
         return;
     }
     if (so.skip_own && D) {
         for (int d = d0 + wv; d < d1; d += step) {
             const size_t off = (bk * Dc + d) * static_cast<size_t>(L) + t;
-            y[off] = from_f32<Tout>(__builtin_fmaf(D[static_cast<size_t>(k) * Dc + d],
-                                                   to_f32(u[off]), yt));
+            store_out<kNt>(y + off, from_f32<Tout>(__builtin_fmaf(
+                                        D[static_cast<size_t>(k) * Dc + d], to_f32(u[off]), yt)));
         }
         return;
     }
     const Tout o = from_f32<Tout>(yt);
-    for (int d = d0 + wv; d < d1; d += step) y[(bk * Dc + d) * static_cast<size_t>(L) + t] = o;
+    for (int d = d0 + wv; d < d1; d += step)
+        store_out<kNt>(y + (bk * Dc + d) * static_cast<size_t>(L) + t, o);
 }
 
 // Reduce stage of one chunk (chunk blockIdx.x / groups of sequence
@@ -487,7 +488,7 @@ __device__ __forceinline__ void get_pair(float* p, float& a, float& b) {
     b = __uint_as_float(static_cast<unsigned>(v >> 32));
 }
 
-template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw>
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw, bool kNt>
 __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
@@ -584,7 +585,7 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     if constexpr (kTwoD) {
         if (wv == 0) ws.ytil[bk * L + t] = yt;
     } else {
-        store_reduced<Tin, Tout>(yt, y, u, D, so, bk, k, Dc, L, t, wv, kRedWaves, 0, Dc);
+        store_reduced<Tin, Tout, kNt>(yt, y, u, D, so, bk, k, Dc, L, t, wv, kRedWaves, 0, Dc);
     }
 }
 
@@ -653,7 +654,7 @@ __device__ __forceinline__ void ch_partials(const MeanWs& ws, const Tin* __restr
 // channels (lane-contiguous rows).
 // With kTwoD the reduced sequence itself is stored (to ws.ytil) for the
 // merge-and-broadcast pass.
-template <int N, typename Tin, typename Tout, bool kTwoD>
+template <int N, typename Tin, typename Tout, bool kTwoD, bool kNt>
 __global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(
     MeanWs ws, const Tin* __restrict__ Cm, Tout* __restrict__ y, const Tin* __restrict__ u,
     const float* __restrict__ D, int K, int Dc, int L, int C, int nchunks, int groups,
@@ -682,7 +683,7 @@ __global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(
         return;
     }
     const int dg0 = (grp * Dc) / groups, dg1 = ((grp + 1) * Dc) / groups;
-    store_reduced<Tin, Tout>(yt, y, u, D, so, bk, k, Dc, L, t, wv, kFinWaves, dg0, dg1);
+    store_reduced<Tin, Tout, kNt>(yt, y, u, D, so, bk, k, Dc, L, t, wv, kFinWaves, dg0, dg1);
 }
 
 // 2-D layout: fold the four reduced sequences of each batch element into one
@@ -691,7 +692,7 @@ __global__ __launch_bounds__(kC* kFinWaves) void k_mean_finish_seq(
 // With a per-channel skip (x given) each channel adds the merge of its four
 // directions' D[k, d] x[b, d, pixel] terms, (D0 + D2) + (D1 + D3) times x.
 // grid: (block of 256 pixels, channel groups, batch).
-template <typename Tin, typename Tout>
+template <typename Tin, typename Tout, bool kNt>
 __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __restrict__ ytil,
                                                               Tout* __restrict__ y,
                                                               const Tin* __restrict__ x,
@@ -713,13 +714,14 @@ __global__ __launch_bounds__(256) void k_mean_merge_broadcast(const float* __res
         const Tin* xp = x + static_cast<size_t>(b) * Dc * L + p;
         for (int d = dg0; d < dg1; ++d) {
             const float dsum = (D[d] + D[2 * Dc + d]) + (D[Dc + d] + D[3 * Dc + d]);
-            yp[static_cast<size_t>(d) * L] =
-                from_f32<Tout>(__builtin_fmaf(dsum, to_f32(xp[static_cast<size_t>(d) * L]), ym));
+            store_out<kNt>(yp + static_cast<size_t>(d) * L,
+                           from_f32<Tout>(__builtin_fmaf(dsum, to_f32(xp[static_cast<size_t>(d) * L]),
+                                                         ym)));
         }
         return;
     }
     const Tout o = from_f32<Tout>(ym);
-    for (int d = dg0; d < dg1; ++d) yp[static_cast<size_t>(d) * L] = o;
+    for (int d = dg0; d < dg1; ++d) store_out<kNt>(yp + static_cast<size_t>(d) * L, o);
 }
 
 // Channel groups for a broadcast pass: the wanted count, at least 1 and at
@@ -737,9 +739,11 @@ vmb_status launch_merge_broadcast(const float* ytil, const ScanArgs& a) {
     const int mgroups = clamp_groups(mwant, Dc);
     // per-channel skip: x and D (an absent D makes it the reduced output alone)
     const bool own = (a.options & VMB_MEAN_SKIP_PER_CHANNEL) && a.D;
-    hipLaunchKernelGGL((k_mean_merge_broadcast<Tin, Tout>),
-                       dim3(pblk, static_cast<unsigned>(mgroups), unsigned(a.batch)), dim3(256), 0,
-                       a.stream, ytil, static_cast<Tout*>(a.y),
+    // non-temporal stores for planes of whole cache lines
+    auto kernel = whole_lines(L, sizeof(Tout)) ? k_mean_merge_broadcast<Tin, Tout, true>
+                                               : k_mean_merge_broadcast<Tin, Tout, false>;
+    hipLaunchKernelGGL(kernel, dim3(pblk, static_cast<unsigned>(mgroups), unsigned(a.batch)),
+                       dim3(256), 0, a.stream, ytil, static_cast<Tout*>(a.y),
                        own ? static_cast<const Tin*>(a.u) : nullptr, a.D, Dc, H, W, mgroups);
     return check_launch();
 }
@@ -976,7 +980,7 @@ vmb_status run(const ScanArgs& a) {
     if constexpr (!kZoh) {
         if (fused && nchunks > 1) {
             const long long cap = resident_workgroups(
-                reinterpret_cast<const void*>(&k_mean_fused<N, Tin, Tout, kTwoD, kRaw>),
+                reinterpret_cast<const void*>(&k_mean_fused<N, Tin, Tout, kTwoD, kRaw, false>),
                 kC * kRedWaves);
             if (cap < 1) return VMB_ERR_HIP;
             fused = wgs <= kFusedRounds * cap;
@@ -997,8 +1001,12 @@ vmb_status run(const ScanArgs& a) {
     so.skip_own = (a.options & VMB_MEAN_SKIP_PER_CHANNEL) ? 1 : 0;
     so.no_bcast = (a.options & VMB_MEAN_NO_BROADCAST) ? 1 : 0;
     if constexpr (!kZoh) if (fused) {
-        hipLaunchKernelGGL((k_mean_fused<N, Tin, Tout, kTwoD, kRaw>), grid, dim3(kC * kRedWaves),
-                           0, a.stream, static_cast<const Tin*>(a.u),
+        // non-temporal broadcast stores for rows of whole cache lines (N = 16)
+        auto kernel = (N == 16 && !kTwoD && whole_lines(L, sizeof(Tout)))
+                          ? k_mean_fused<N, Tin, Tout, kTwoD, kRaw, N == 16 && !kTwoD>
+                          : k_mean_fused<N, Tin, Tout, kTwoD, kRaw, false>;
+        hipLaunchKernelGGL(kernel, grid, dim3(kC * kRedWaves), 0, a.stream,
+                           static_cast<const Tin*>(a.u),
                            static_cast<const Tin*>(a.delta), a.A, static_cast<const Tin*>(a.B),
                            static_cast<const Tin*>(a.C), a.D, a.dt_bias, xt, ws,
                            reinterpret_cast<unsigned long long*>(p + lay.flags), stat,
@@ -1039,8 +1047,10 @@ vmb_status run(const ScanArgs& a) {
     const long long seqs = a.batch * a.K;
     const long long want = (512 + nblk * seqs - 1) / (nblk * seqs);
     const int groups = kTwoD || so.no_bcast ? 1 : clamp_groups(want, Dc);
-    hipLaunchKernelGGL((k_mean_finish_seq<N, Tin, Tout, kTwoD>),
-                       dim3(nblk, static_cast<unsigned>(a.K * groups), unsigned(a.batch)),
+    auto fin = (N == 16 && !kTwoD && whole_lines(L, sizeof(Tout)))
+                   ? k_mean_finish_seq<N, Tin, Tout, kTwoD, N == 16 && !kTwoD>
+                   : k_mean_finish_seq<N, Tin, Tout, kTwoD, false>;
+    hipLaunchKernelGGL(fin, dim3(nblk, static_cast<unsigned>(a.K * groups), unsigned(a.batch)),
                        dim3(kC * kFinWaves), 0, a.stream, ws, static_cast<const Tin*>(a.C),
                        static_cast<Tout*>(a.y), static_cast<const Tin*>(a.u), a.D, K, Dc, L, C,
                        nchunks, groups, inline_carry, so);
