@@ -22,7 +22,9 @@
 // runs in its kernel). Per (position, state): mul, exp2, mul, 3 fma.
 //
 // States go in pairs, one workgroup barrier per pair: phase 1 (steps 1-2 up
-// to the wave's aggregate) before it, the cross-wave join and phase 2 after.
+// to the wave's aggregate) before it, the cross-wave join and phase 2 after;
+// the two states' chains are interleaved, which gives each wave two
+// independent dependency chains to issue from.
 // B and C rows are shared by every channel of a direction. Four copy waves
 // move each pair's slices of them once, straight from global memory into LDS
 // (global_load_lds), double-buffered: before barrier p they issue C of pair p
@@ -190,41 +192,51 @@ __device__ __forceinline__ void load_run_2d_global(const Tin* plane, int k, int 
     load_run_2d<T>(plane, k, t0, H, W, L, v, cnt);
 }
 
-// Phase 1 of one state for one lane: a_i, b_i of its run (registers), the
-// run aggregate, the inclusive scan over the wave (Pin, Hin, kept for phase
-// 2), and this wave's aggregate published by the last lane to xg[slot]
-// (the channel's row, see state_phase2).
-// With kZoh, Bbar u takes the zero-order-hold form (zoh_q, from the run's u
-// values uvr and inv_an = 1 / A_n) instead of Delta u.
+// Phase 1 of a pair of states (an0, an1) for one lane: per state, a_i and
+// b_i of its run (registers), the run aggregate, the inclusive scan over the
+// wave (Pin, Hin, kept for phase 2), and this wave's aggregate published by
+// the last lane to xg[slot] (the channel's row, see lane_entry). The two
+// states' chains are interleaved (their aggregates and wave scans are
+// independent). With kZoh, Bbar u takes the zero-order-hold form (zoh_q,
+// from the run's u values uvr and inv = 1 / A_n) instead of Delta u.
 template <int T, typename Tin, bool kZoh = false>
-__device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], const float (&du)[T],
-                                             float s2, const Tin* bsrc, float (&a)[T],
-                                             float (&bu)[T], float& Pin, float& Hin,
-                                             float (*xg)[2], int lane, int slot,
-                                             const float (&uvr)[T], float inv_an) {
-    float agg = 0.0f;
+__device__ __forceinline__ void pair_phase1(float an0, float an1, const float (&dl2)[T],
+                                            const float (&du)[T], float s2, const Tin* b0src,
+                                            const Tin* b1src, float (&a0)[T], float (&bu0)[T],
+                                            float (&a1)[T], float (&bu1)[T], float& Pin0,
+                                            float& Hin0, float& Pin1, float& Hin1,
+                                            float (*xg0)[2], float (*xg1)[2], int lane, int slot,
+                                            const float (&uvr)[T], float inv0, float inv1) {
+    float agg0 = 0.0f, agg1 = 0.0f;
 #pragma unroll
     for (int i = 0; i < T; ++i) {
-        const float x2 = dl2[i] * an;
-        a[i] = fast_exp2(x2);
-        const float q = kZoh ? zoh_q(x2, a[i], du[i], uvr[i], inv_an) : du[i];
-        bu[i] = q * to_f32(bsrc[i]);
-        agg = i == 0 ? bu[0] : __builtin_fmaf(a[i], agg, bu[i]);
+        const float x0 = dl2[i] * an0, x1 = dl2[i] * an1;
+        a0[i] = fast_exp2(x0);
+        a1[i] = fast_exp2(x1);
+        const float q0 = kZoh ? zoh_q(x0, a0[i], du[i], uvr[i], inv0) : du[i];
+        const float q1 = kZoh ? zoh_q(x1, a1[i], du[i], uvr[i], inv1) : du[i];
+        bu0[i] = q0 * to_f32(b0src[i]);
+        bu1[i] = q1 * to_f32(b1src[i]);
+        agg0 = i == 0 ? bu0[0] : __builtin_fmaf(a0[i], agg0, bu0[i]);
+        agg1 = i == 0 ? bu1[0] : __builtin_fmaf(a1[i], agg1, bu1[i]);
     }
-    Pin = fast_exp2(s2 * an);
-    Hin = agg;
-    wave_scan(Pin, Hin);
+    Pin0 = fast_exp2(s2 * an0);
+    Pin1 = fast_exp2(s2 * an1);
+    Hin0 = agg0;
+    Hin1 = agg1;
+    wave_scan2(Pin0, Hin0, Pin1, Hin1);
     if (lane == kWave - 1) {
-        xg[slot][0] = Pin;
-        xg[slot][1] = Hin;
+        xg0[slot][0] = Pin0;
+        xg0[slot][1] = Hin0;
+        xg1[slot][0] = Pin1;
+        xg1[slot][1] = Hin1;
     }
 }
 
-// Phase 2 (after the workgroup barrier): state entering this wave from the
-// channel's earlier waves and the previous chunk (*hcar, this wave's own copy
-// of the carry), the state entering this lane (lane - 1's inclusive scan
-// applied to it, read across lanes), then the re-walk of the run,
-// accumulating y_i += C_i h_i.
+// Phase 2 (after the workgroup barrier), first part, for one state: the
+// state entering this wave from the channel's earlier waves and the previous
+// chunk (*hcar, this wave's own copy of the carry), then the state entering
+// this lane (lane - 1's inclusive scan applied to it, read across lanes).
 //
 // xg is the channel's row of slots. With kCarryOut (chunks pass a carry on)
 // it holds the aggregates of waves 0 .. kWv - 1; every wave composes all of
@@ -233,10 +245,9 @@ __device__ __forceinline__ void state_phase1(float an, const float (&dl2)[T], co
 // the row starts with kWv - 1 identities (1, 0) and wave w composes the
 // kWv - 1 slots from w on (identities, then waves 0 .. w - 1): the same
 // count of steps for every wave, with no per-wave selection.
-template <int T, int kWv, bool kCarryOut, typename Tin>
-__device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&bu)[T], float Pin,
-                                             float Hin, const Tin* csrc, float (&yv)[T],
-                                             const float (*xg)[2], float* hcar, int lane, int w) {
+template <int kWv, bool kCarryOut>
+__device__ __forceinline__ float lane_entry(float Pin, float Hin, const float (*xg)[2],
+                                            float* hcar, int lane, int w) {
     const float hc = *hcar;
     float cin = hc;
     if constexpr (kCarryOut) {
@@ -256,14 +267,29 @@ __device__ __forceinline__ void state_phase2(const float (&a)[T], const float (&
         }
     }
     // lane 0 starts from cin itself (the shift leaves its old value)
-    float h = dpp<kWaveShr1, 0xf>(cin, __builtin_fmaf(Pin, cin, Hin));
+    return dpp<kWaveShr1, 0xf>(cin, __builtin_fmaf(Pin, cin, Hin));
+}
+
+// Phase 2 of the pair: both re-walks from the lanes' entering states,
+// interleaved, accumulating y_i += C0_i h0_i, then += C1_i h1_i. The end of
+// the re-walk is pinned here: left to itself the compiler sinks it past the
+// next step's phase 1, which then needs two steps' run arrays at once.
+template <int T, int kWv, bool kCarryOut, typename Tin>
+__device__ __forceinline__ void pair_phase2(const float (&a0)[T], const float (&bu0)[T],
+                                            const float (&a1)[T], const float (&bu1)[T],
+                                            float Pin0, float Hin0, float Pin1, float Hin1,
+                                            const Tin* c0src, const Tin* c1src, float (&yv)[T],
+                                            const float (*xg0)[2], const float (*xg1)[2],
+                                            float* hcar0, float* hcar1, int lane, int w) {
+    float h0 = lane_entry<kWv, kCarryOut>(Pin0, Hin0, xg0, hcar0, lane, w);
+    float h1 = lane_entry<kWv, kCarryOut>(Pin1, Hin1, xg1, hcar1, lane, w);
 #pragma unroll
     for (int i = 0; i < T; ++i) {
-        h = __builtin_fmaf(a[i], h, bu[i]);
-        yv[i] = __builtin_fmaf(to_f32(csrc[i]), h, yv[i]);
+        h0 = __builtin_fmaf(a0[i], h0, bu0[i]);
+        h1 = __builtin_fmaf(a1[i], h1, bu1[i]);
+        yv[i] = __builtin_fmaf(to_f32(c0src[i]), h0, yv[i]);
+        yv[i] = __builtin_fmaf(to_f32(c1src[i]), h1, yv[i]);
     }
-    // finish the re-walk here: left to itself the compiler sinks it past the
-    // next step's phase 1, which then needs two steps' run arrays at once
 #pragma unroll
     for (int i = 0; i < T; ++i) asm volatile("" : "+v"(yv[i]));
 }
@@ -366,7 +392,7 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
     constexpr int kPairs = N / 2;
     constexpr int G = kComputeWaves / kWv;  // channels per workgroup
     // per (parity, state of the pair, channel): aggregates exchanged across
-    // waves, after kLead identity slots (see state_phase2)
+    // waves, after kLead identity slots (see lane_entry)
     constexpr int kLead = kOne ? kWv - 1 : 0;  // identity slots before the waves'
     constexpr int kSlots = kLead + kWv;
     __shared__ __align__(16) float xagg[2][2][G][kSlots][2];
@@ -521,15 +547,13 @@ __global__ __launch_bounds__(kStageThreads) void k_full_scan_chunked(
             const float inv0 = kZoh ? 1.0f / a01.x : 0.0f, inv1 = kZoh ? 1.0f / a01.y : 0.0f;
             float a0[T], bu0[T], a1[T], bu1[T];
             float Pin0, Hin0, Pin1, Hin1;
-            state_phase1<T, Tin, kZoh>(a01.x, dl2, du, s2, &bcur[0][run], a0, bu0, Pin0, Hin0,
-                                       xq[0][g], lane, kLead + w, uv, inv0);
-            state_phase1<T, Tin, kZoh>(a01.y, dl2, du, s2, &bcur[1][run], a1, bu1, Pin1, Hin1,
-                                       xq[1][g], lane, kLead + w, uv, inv1);
+            pair_phase1<T, Tin, kZoh>(a01.x, a01.y, dl2, du, s2, &bcur[0][run], &bcur[1][run], a0,
+                                      bu0, a1, bu1, Pin0, Hin0, Pin1, Hin1, xq[0][g], xq[1][g],
+                                      lane, kLead + w, uv, inv0, inv1);
             __syncthreads();
-            state_phase2<T, kWv, kOut>(a0, bu0, Pin0, Hin0, &ccur[0][run], yv, xq[0][g],
-                                       &hcar[wv][n0], lane, w);
-            state_phase2<T, kWv, kOut>(a1, bu1, Pin1, Hin1, &ccur[1][run], yv, xq[1][g],
-                                       &hcar[wv][n0 + 1], lane, w);
+            pair_phase2<T, kWv, kOut>(a0, bu0, a1, bu1, Pin0, Hin0, Pin1, Hin1, &ccur[0][run],
+                                      &ccur[1][run], yv, xq[0][g], xq[1][g], &hcar[wv][n0],
+                                      &hcar[wv][n0 + 1], lane, w);
         };
 #pragma unroll 1
         for (int q = 0; q < kPairs; q += 2) {
