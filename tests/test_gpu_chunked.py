@@ -52,7 +52,9 @@ def test_bf16(out, H, W):
     assert_close(to_f64(y), ref, **(BF16_TOL if out == "bf16" else FP32_TOL), what=f"bf16->{out}")
 
 
-@pytest.mark.parametrize("H,W", [(56, 56), (29, 31), (1, 700), (700, 1), (64, 130)])
+# one chunk (56x56, 29x31, 1x700, 700x1) and several (64x130; 61x67 and 57x64 with whole and
+# partial row-major runs read as vectors, the column-major directions from the plane copies)
+@pytest.mark.parametrize("H,W", [(56, 56), (29, 31), (1, 700), (700, 1), (64, 130), (61, 67), (57, 64)])
 def test_2d_layout(H, W):
     log(f"chunked full 2d {H}x{W}")
     inp = workloads.make_inputs(shape(1, H, W, 4, seed=H * 1000 + W), "2d")
@@ -60,6 +62,17 @@ def test_2d_layout(H, W):
     ref, scale = merged_oracle(inp, "full")
     assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
                  what=f"2d {H}x{W}")
+
+
+# bf16 inputs in the 2-D layout, one chunk and several
+@pytest.mark.parametrize("H,W", [(40, 50), (60, 70)])
+def test_2d_layout_bf16(H, W):
+    log(f"chunked full 2d bf16 {H}x{W}")
+    inp = workloads.make_inputs(shape(1, H, W, 3, "bf16", seed=H * 1000 + W + 7), "2d")
+    got = to_f64(run_scan(inp, "full", "2d", out_dtype=torch.float32))
+    ref, scale = merged_oracle(inp, "full")
+    assert_close(got, ref, rtol=FP32_TOL["rtol"], atol=4 * FP32_TOL["atol"], scale=scale,
+                 what=f"2d bf16 {H}x{W}")
 
 
 def test_softplus_off_and_no_bias():
