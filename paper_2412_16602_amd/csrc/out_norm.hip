@@ -19,9 +19,10 @@
 // tensor is in flight and HBM is read once; the mean and the centred sum of
 // squares (exact in fp32 for any offset of the mean) are then formed from
 // the registers. Wider channel counts stream the channels three times (the
-// second and third reads from cache). The group sums meet in LDS in group
-// order (deterministic). As in the projections, the 1-D grid is dealt to the
-// XCDs in contiguous ranges of tiles, so neighbouring tiles, which share the
+// second and third reads from cache). The group sums are added across each
+// wave by shuffles, then the waves' sums in LDS in wave order
+// (deterministic). As in the projections, the 1-D grid is dealt to the XCDs
+// in contiguous ranges of tiles, so neighbouring tiles, which share the
 // 128-byte lines of a channel row, read them through one L2.
 #include "vmb_internal.h"
 
@@ -30,15 +31,23 @@ namespace {
 
 constexpr int kThreads = 1024;
 
-// Sum of v over the channel groups of this thread's pixel, in group order.
+// Sum of v over the channel groups of this thread's pixel, in a fixed order:
+// a wave holds 64 / PX groups of the same PX pixels (lane l: pixel l % PX),
+// which are first added across the wave (xor shuffles over the lane bits
+// above the pixel's), then the waves' sums in wave order.
 template <int PX>
 __device__ __forceinline__ float group_total(float (*red)[PX + 1], float* tot, float v, int px,
                                              int grp) {
-    red[grp][px] = v;
+    constexpr int kWave = 64, kWaves = kThreads / kWave;
+#pragma unroll
+    for (int m = PX; m < kWave; m *= 2) v += __shfl_xor(v, m, kWave);
+    const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+    if (lane < PX) red[wv][px] = v;
     __syncthreads();
     if (grp == 0) {
         float t = 0.0f;
-        for (int g = 0; g < kThreads / PX; ++g) t += red[g][px];
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) t += red[w][px];
         tot[px] = t;
     }
     __syncthreads();
