@@ -11,9 +11,9 @@
 // Passes over chunks of C = 64 positions:
 //   1. reduce : a workgroup owns one chunk of one (batch, k); lanes own
 //               positions (coalesced loads along t), each of its 16 waves sums
-//               a fixed sixteenth of the channels (their parameters staged in
+//               a fixed share of the channels (their parameters staged in
 //               the wave's LDS slice and read as broadcasts; delta / u of the
-//               next channels in flight), and the sixteenths are added in a
+//               next channels in flight), and the shares are added in a
 //               fixed order in LDS. Each state's
 //               chunk-local inclusive scan of the pairs (Abar_mean, B s_mean),
 //               composed with (a1, b1) then (a2, b2) -> (a1 a2, a2 b1 + b2), is
@@ -44,6 +44,14 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kC = kMeanChunk;  // positions per chunk = lanes per wave
 constexpr int kRedWaves = 16;   // channel split of the reduce pass
+// Channel shares of the reduce waves by age on their SIMD (waves w, w + 4,
+// w + 8, w + 12 share SIMD w): the SIMD issues the oldest ready wave first,
+// so with equal shares the youngest waves finish last and run alone at the
+// end. Older waves take more channels (15 : 13 : 11 : 9 of every 48); the
+// split is fixed, so the sums keep their order from call to call.
+constexpr int kShareW[4] = {15, 13, 11, 9};
+constexpr int kShareTot = 4 * (kShareW[0] + kShareW[1] + kShareW[2] + kShareW[3]);
+static_assert(kRedWaves == 16, "four waves of each age rank, one per SIMD");
 constexpr int kAhead = 4;       // channels of delta / u in flight per wave
 
 __device__ float g_zero = 0.0f;  // stands in for an absent dt_bias / D (never written)
@@ -146,8 +154,20 @@ __device__ __forceinline__ void reduce_partials(
 #pragma unroll
     for (int n = 0; n < (kZoh ? N : 1); ++n) zacc[n] = 0.0f;
     float s = 0.0f, r = 0.0f, q = 0.0f;
-    const int slice = grp * kRedWaves + wv, nslices = kRedWaves * groups;
-    const int d0 = (slice * Dc) / nslices, d1 = ((slice + 1) * Dc) / nslices;
+    // channels [d0, d1) of this wave: with one group the age-weighted shares
+    // (kShareW), with several (the split reduce) equal shares of the group
+    int d0, d1;
+    if (groups == 1) {
+        const int rank = wv / 4;
+        int cum = (wv % 4) * kShareW[rank];
+        for (int r = 0; r < rank; ++r) cum += 4 * kShareW[r];
+        d0 = (cum * Dc) / kShareTot;
+        d1 = ((cum + kShareW[rank]) * Dc) / kShareTot;
+    } else {
+        const int slice = grp * kRedWaves + wv, nslices = kRedWaves * groups;
+        d0 = (slice * Dc) / nslices;
+        d1 = ((slice + 1) * Dc) / nslices;
+    }
     const int nw = d1 - d0;  // channels of this wave
     float* prm = &part[wv][0][0];
     const size_t cw = static_cast<size_t>(k) * Dc + d0;  // parameter row of the wave's first channel
