@@ -335,10 +335,6 @@ vmb_status launch_scan_planes(const void* x, void* xs, int64_t batch, int64_t ch
 
 }  // namespace
 
-bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
-    return plane_fits(batch, channels, H, W);
-}
-
 bool cross_fits(int64_t batch, int64_t channels, int64_t H, int64_t W) {
     return plane_fits(batch, channels, H, W) || grid_fits(batch, channels, H, W);
 }

@@ -930,7 +930,7 @@ vmb_status run_pooled(const ScanArgs& a) {
     const int C = kC;
     const int nchunks = (L + C - 1) / C;
     const Tin* xt = nullptr;
-    if (kTwoD && mean_transposes(a.L, true) && cross_plane_fits(a.batch, a.channels, a.H, a.W)) {
+    if (kTwoD && mean_transposes(a.L, true) && cross_fits(a.batch, a.channels, a.H, a.W)) {
         vmb_status s0 = launch_transpose_planes(a.u, p + lay.xt, a.batch, a.channels, a.H, a.W,
                                                 a.in_dt, a.stream);
         if (s0 != VMB_OK) return s0;
@@ -1011,7 +1011,7 @@ vmb_status run(const ScanArgs& a) {
     // 2-D layout: column-major copies of the planes first, so that every
     // direction's reduce reads stay coalesced
     const Tin* xt = nullptr;
-    if (kTwoD && mean_transposes(a.L, true) && cross_plane_fits(a.batch, a.channels, a.H, a.W)) {
+    if (kTwoD && mean_transposes(a.L, true) && cross_fits(a.batch, a.channels, a.H, a.W)) {
         vmb_status s0 = launch_transpose_planes(a.u, p + lay.xt, a.batch, a.channels, a.H, a.W,
                                                 a.in_dt, a.stream);
         if (s0 != VMB_OK) return s0;

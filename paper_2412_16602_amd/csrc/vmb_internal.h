@@ -98,21 +98,21 @@ struct MeanStatus {
 //   agg   [bk][nch][N][2]     : chunk aggregates
 //   carry [bk][nch][N]        : state entering each chunk
 //   ytil  [bk][L]             : 2-D layout only, the reduced output
-//   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL only,
+//   xt    [batch*channels][L] : 2-D layout with L >= kMeanTransposeMinL only,
 //                               column-major copies of the input planes
 //   flags [bk][nch]     u64   : one-launch path's chunk flags
 //   gpart [bk][nch][G][2N+3][64] : with G = mean_groups(..) > 1 only, each
 //                               channel group's partial sums of a chunk
-constexpr int64_t kMeanTransposeMaxL = 6144;  // then H * (W + 1) <= 2 L fits LDS
-static_assert(kMeanTransposeMaxL == 6144, "full_ws_has_xt uses the same bound");
 struct MeanWsLayout {
     size_t scan, rmean, agg, carry, ytil, xt, flags, gpart, total;
 };
 // Short planes (a few cache lines) are gathered directly instead: the copy
-// pass costs more than it saves there.
+// pass costs more than it saves there. Planes beyond LDS are copied in 32 x 32
+// tiles (2 x 128 x 512: the copy takes 55 us, the column gathers it replaces
+// about 200 us of the reduce).
 constexpr int64_t kMeanTransposeMinL = 256;
 inline bool mean_transposes(int64_t L, bool two_d) {
-    return two_d && L >= kMeanTransposeMinL && L <= kMeanTransposeMaxL;
+    return two_d && L >= kMeanTransposeMinL;
 }
 inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, int64_t L,
                                    int64_t N, bool two_d) {
@@ -143,7 +143,7 @@ inline MeanWsLayout mean_ws_layout(int64_t batch, int64_t K, int64_t channels, i
 //   ones  [batch][L]   : the scan's output coefficient (its states are wanted as they are)
 //   rbar  [batch][L]   : pooled skip term
 //   ytil  [batch][4][L]: ytilde written once per direction (2-D merge input)
-//   xt    [batch*channels][L] : 2-D layout with L <= kMeanTransposeMaxL, as in the main reading
+//   xt    [batch*channels][L] : 2-D layout with L >= kMeanTransposeMinL, as in the main reading
 // after the completion record (kMeanStatusBytes).
 struct PooledWsLayout {
     size_t psum, abar, bu, cbar, h, ones, rbar, ytil, xt, total;
@@ -170,12 +170,11 @@ inline PooledWsLayout pooled_ws_layout(int64_t batch, int64_t K, int64_t channel
 // Launchers (enqueue only; arguments already validated).
 vmb_status launch_cross_scan(const void* x, void* xs, int64_t batch, int64_t channels,
                              int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);
-// Column-major copy of every (batch, channel) plane, xt[plane][w * H + h]
-// (direction 1's sequence); only for planes that cross_plane_fits accepts.
-bool cross_plane_fits(int64_t batch, int64_t channels, int64_t H, int64_t W);
 // Whether the cross-scan / merge kernels take the map at all (a plane in LDS,
 // or 32 x 32 tiles within the grid limits); checked before any launch.
 bool cross_fits(int64_t batch, int64_t channels, int64_t H, int64_t W);
+// Column-major copy of every (batch, channel) plane, xt[plane][w * H + h]
+// (direction 1's sequence), for any plane cross_fits accepts.
 vmb_status launch_transpose_planes(const void* x, void* xt, int64_t batch, int64_t channels,
                                    int64_t H, int64_t W, vmb_dtype dt, hipStream_t s);
 // Merge with independent input / output element types (fp32 -> bf16 is used
