@@ -124,12 +124,33 @@ def gpu_bench(args):
                layout=lay, workspace=d["ws"], stream=stream)
         return call
 
+    # The stream is idle after the synchronize that ends the warmup. With
+    # nothing queued ahead of the start event, the host-side marshalling and
+    # launch of the first timed call (about 15 us on the GPU host, against
+    # about 25 us of device time per call) would be timed as device idle: a
+    # 20-step run read 27.1 us per call where 200 steps read 25.9. A device
+    # sleep of about 60 us is queued before the start event, so the timed
+    # region starts with the first calls already queued; the later calls are
+    # still enqueued at the host's own rate, so a host slower than the device
+    # would still show in the result.
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    probe = 1 << 20
+    torch.cuda._sleep(probe)  # first use (module load) outside the measurement
+    torch.cuda.synchronize()
+    e0.record(stream)
+    torch.cuda._sleep(probe)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    lead_cycles = max(1, int(probe * 60.0 / (e0.elapsed_time(e1) * 1e3)))
+
     def timed(call, steps, warmup):
         for i in range(warmup):
             call(i)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(lead_cycles)
         e0.record(stream)
         for i in range(steps):
             call(i)
