@@ -274,14 +274,46 @@ __global__ __launch_bounds__(256) void k_projections(
     const float* Wd = Wdt + static_cast<size_t>(k) * Dc * R;
     constexpr int RS = kMaxR / 4;
     float* swd = pool;
+    // With a wide x_dbl block (MB >= 4: rank 17 or more at N = 16) the next
+    // chunk of W_dt is loaded into registers while the current one is in
+    // use: at rank 48 (7x7 stage, 1536 channels) each chunk is 12 KB and the
+    // product over it is short, so a load that waits before every chunk left
+    // the matrix cores idle most of the time. At low ranks the chunk is a
+    // few hundred bytes and the extra registers cost more than they hide.
+    constexpr bool kPrefetch = MB >= 4;
+    constexpr int kPf = kPrefetch ? (kDC * kMaxR) / 256 : 1;
+    float pf[kPf];
+    auto fetch = [&](int d0) {
+        const int n = (Dc - d0 < kDC ? Dc - d0 : kDC) * R;
+#pragma unroll
+        for (int j = 0; j < kPf; ++j) {
+            const int i = tid + 256 * j;
+            pf[j] = i < n ? Wd[static_cast<size_t>(d0) * R + i] : 0.0f;
+        }
+    };
+    if constexpr (kPrefetch) fetch(0);
     for (int d0 = 0; d0 < Dc; d0 += kDC) {
         // W_dt rows d0 .. d0 + 64 are one contiguous block
         const int rows = Dc - d0 < kDC ? Dc - d0 : kDC;
-        for (int i = tid; i < rows * R; i += 256) {
-            const int r = i / R, c = i - r * R;
-            swd[r * kPadR + c] = Wd[static_cast<size_t>(d0) * R + i];
+        if constexpr (kPrefetch) {
+#pragma unroll
+            for (int j = 0; j < kPf; ++j) {
+                const int i = tid + 256 * j;
+                if (i < rows * R) {
+                    const int r = i / R, c = i - r * R;
+                    swd[r * kPadR + c] = pf[j];
+                }
+            }
+        } else {
+            for (int i = tid; i < rows * R; i += 256) {
+                const int r = i / R, c = i - r * R;
+                swd[r * kPadR + c] = Wd[static_cast<size_t>(d0) * R + i];
+            }
         }
         __syncthreads();
+        if constexpr (kPrefetch) {
+            if (d0 + kDC < Dc) fetch(d0 + kDC);  // in flight during this chunk's products
+        }
         const int dl = 16 * wv + col;  // A-operand row (channel within the chunk)
         float a[RS];
 #pragma unroll
