@@ -188,6 +188,11 @@ vmb_status vmb_selective_scan_fwd_ex(const void* u, const void* delta, const flo
  * Arguments, shapes, dtypes and workspace rules are those of
  * vmb_selective_scan_fwd (workspace sized by vmb_scan_workspace_bytes(1, ...)).
  * Channel sums are binary32 in a fixed order (deterministic).
+ * HIP graphs: a call made while `stream` is capturing takes the separate
+ * passes, ordered by kernel boundaries alone (the one-launch form, whose
+ * workgroups wait on per-call flags, would carry one call's flag value into
+ * every replay), so a captured call replayed on new inputs computes the
+ * result for those inputs. The same holds for _ex and _noalloc.
  */
 vmb_status vmb_mean_scan_fwd(const void* u, const void* delta, const float* A, const void* B,
                              const void* C, const float* D, const float* dt_bias,

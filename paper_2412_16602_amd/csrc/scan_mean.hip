@@ -999,6 +999,19 @@ vmb_status run(const ScanArgs& a) {
     bool fused = !kZoh && rgroups == 1 && C == kC && nchunks <= kWave;
     if constexpr (!kZoh) {
         if (fused && nchunks > 1) {
+            // A call captured into a HIP graph keeps its arguments, this
+            // call's flag value included, for every replay: a workgroup could
+            // take an earlier chunk's flag left by the previous replay for this
+            // one's and read that replay's aggregates. Captured calls take the
+            // separate passes, which kernel boundaries alone order.
+            hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+            if (hipStreamIsCapturing(a.stream, &cs) != hipSuccess) {
+                (void)hipGetLastError();  // the separate passes are safe either way
+                cs = hipStreamCaptureStatusActive;
+            }
+            if (cs != hipStreamCaptureStatusNone) fused = false;
+        }
+        if (fused && nchunks > 1) {
             const long long cap = resident_workgroups(
                 reinterpret_cast<const void*>(&k_mean_fused<N, Tin, Tout, kTwoD, kRaw, false>),
                 kC * kRedWaves);
