@@ -53,6 +53,16 @@ constexpr int kShareW[4] = {15, 13, 11, 9};
 constexpr int kShareTot = 4 * (kShareW[0] + kShareW[1] + kShareW[2] + kShareW[3]);
 static_assert(kRedWaves == 16, "four waves of each age rank, one per SIMD");
 constexpr int kAhead = 4;       // channels of delta / u in flight per wave
+// The reduce and one-launch kernels whose LDS lets two workgroups share a CU
+// (at most 80 KB each: all but the zero-order-hold reduce and the one-launch
+// raw-means form) are built for 8 waves per SIMD, i.e. at most 64 VGPRs,
+// with two channels in flight per wave instead of four (the ring of four
+// does not fit 64 registers without spills). Mean calls then take 0.80-0.86
+// of the time at 128 x 56x56 (three passes), 0.85 at 32 x 28x28 (one
+// launch) and 0.88-0.91 at 2 x 128x512; at 1 x 56x56 (196 workgroups)
+// there is no second workgroup to place and the time is unchanged.
+constexpr int kAheadPaired = 2;
+constexpr int kWavesPaired = 8;  // waves per SIMD: two 16-wave workgroups per CU
 
 __device__ float g_zero = 0.0f;  // stands in for an absent dt_bias / D (never written)
 constexpr int kFinWaves = 4;    // waves of a finish workgroup
@@ -117,19 +127,19 @@ constexpr int part_rows() {
     return N + 2 + (kRaw ? 1 : 0) + (kZoh ? N : 0);
 }
 
-template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh = false>
+template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh = false, int kAh = kAhead>
 __device__ __forceinline__ void reduce_partials(
     float (*part)[(part_rows<N, kRaw, kZoh>())][kC], const Tin* __restrict__ u, const Tin* __restrict__ delta,
     const float* __restrict__ A, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, int K, int Dc, int L, int H, int W, int C, int softplus,
     int groups = 1) {
     // Each wave's slice part[wv] first holds its channel parameters (two
-    // buffers of kAhead rows: A[c, 0..N) log2(e), dt_bias[c], D[c], and with
+    // buffers of kAh rows: A[c, 0..N) log2(e), dt_bias[c], D[c], and with
     // kZoh 1 / A[c, 0..N)), read back as wave-uniform broadcasts, and
     // afterwards its partial sums.
     constexpr int kPS = (N + 2 + (kZoh ? N : 0) + 3) & ~3;  // parameter row stride (16-byte rows)
-    static_assert(2 * kAhead * kPS <= (N + 2) * kC, "parameter buffers fit a wave's slice");
-    static_assert(kAhead <= 32, "parameter row layout");
+    static_assert(2 * kAh * kPS <= (N + 2) * kC, "parameter buffers fit a wave's slice");
+    static_assert(kAh <= 32, "parameter row layout");
     const int chunk = blockIdx.x / groups, grp = blockIdx.x % groups;
     const int k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
@@ -187,35 +197,35 @@ __device__ __forceinline__ void reduce_partials(
         dv = to_f32(*reinterpret_cast<const Tin*>(dp + toff));
         uv = to_f32(*reinterpret_cast<const Tin*>(up + soff));
     };
-    // parameters of wave channels i0 .. i0 + kAhead - 1 (clamped): global
+    // parameters of wave channels i0 .. i0 + kAh - 1 (clamped): global
     // loads into registers, later written to LDS buffer buf
-    constexpr int kPA = (kAhead * N + kC - 1) / kC;
+    constexpr int kPA = (kAh * N + kC - 1) / kC;
     auto load_par = [&](int i0, float (&pa)[kPA], float& pbd) {
 #pragma unroll
         for (int m = 0; m < kPA; ++m) {
-            const int idx = (lane + m * kC) % (kAhead * N);
+            const int idx = (lane + m * kC) % (kAh * N);
             const int i = i0 + idx / N;
             pa[m] = A[(cw + (i < nw ? i : nw - 1)) * N + idx % N];
         }
-        const int i = i0 + (lane % kAhead);
+        const int i = i0 + (lane % kAh);
         const size_t c = cw + (i < nw ? i : nw - 1);
         pbd = lane < 32 ? pbias[c * bias_stride] : pskip[c * skip_stride];
     };
     auto write_par = [&](int buf, const float (&pa)[kPA], float pbd) {
-        float* base = prm + buf * kAhead * kPS;
+        float* base = prm + buf * kAh * kPS;
 #pragma unroll
         for (int m = 0; m < kPA; ++m) {
             const int idx = lane + m * kC;
-            if (idx < kAhead * N) {
+            if (idx < kAh * N) {
                 base[(idx / N) * kPS + idx % N] = pa[m] * kLog2e;
                 if constexpr (kZoh) base[(idx / N) * kPS + N + 2 + idx % N] = 1.0f / pa[m];
             }
         }
-        if (lane < kAhead) base[lane * kPS + N] = pbd;
-        else if (lane >= 32 && lane < 32 + kAhead) base[(lane - 32) * kPS + N + 1] = pbd;
+        if (lane < kAh) base[lane * kPS + N] = pbd;
+        else if (lane >= 32 && lane < 32 + kAh) base[(lane - 32) * kPS + N + 1] = pbd;
     };
     auto read_par = [&](int buf, int i, float (&an)[N], float& bias, float& dskip) {
-        const float* row = prm + buf * kAhead * kPS + i * kPS;
+        const float* row = prm + buf * kAh * kPS + i * kPS;
 #pragma unroll
         for (int n = 0; n < N; ++n) an[n] = row[n];
         bias = row[N];
@@ -223,7 +233,7 @@ __device__ __forceinline__ void reduce_partials(
     };
     // 1 / A of the same channel (kZoh)
     auto read_inv = [&](int buf, int i, int n) {
-        return prm[buf * kAhead * kPS + i * kPS + N + 2 + n];
+        return prm[buf * kAh * kPS + i * kPS + N + 2 + n];
     };
     auto channel = [&](const float (&an)[N], float bias, float dskip, float dv, float uv, int buf,
                        int i) {
@@ -266,38 +276,38 @@ __device__ __forceinline__ void reduce_partials(
     };
 
     if (nw > 0) {
-        // parameters of the first block, then delta / u of its kAhead
-        // channels: a ring refilled kAhead channels ahead of use
+        // parameters of the first block, then delta / u of its kAh
+        // channels: a ring refilled kAh channels ahead of use
         float pa[kPA], pbd;
         load_par(0, pa, pbd);
         // issued before the ring's loads, so that writing them out waits for
         // them alone
         __builtin_amdgcn_sched_barrier(0);
-        float dv[kAhead], uv[kAhead];
+        float dv[kAh], uv[kAh];
 #pragma unroll
-        for (int j = 0; j < kAhead; ++j) load_ch(j, dv[j], uv[j]);
+        for (int j = 0; j < kAh; ++j) load_ch(j, dv[j], uv[j]);
         write_par(0, pa, pbd);
-        const int nb = nw / kAhead;  // full blocks; the rest is the tail
+        const int nb = nw / kAh;  // full blocks; the rest is the tail
         for (int blk = 0; blk < nb; ++blk) {
-            const int buf = blk & 1, i0 = blk * kAhead;
-            load_par(i0 + kAhead, pa, pbd);
+            const int buf = blk & 1, i0 = blk * kAh;
+            load_par(i0 + kAh, pa, pbd);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int j = 0; j < kAhead; ++j) {
+            for (int j = 0; j < kAh; ++j) {
                 // one channel at a time (no hoisting across channels, which
                 // would cost registers the load ring needs)
                 __builtin_amdgcn_sched_barrier(0);
                 float an[N], bias, dskip;
                 read_par(buf, j, an, bias, dskip);
                 channel(an, bias, dskip, dv[j], uv[j], buf, j);
-                load_ch(i0 + kAhead + j, dv[j], uv[j]);
+                load_ch(i0 + kAh + j, dv[j], uv[j]);
             }
             __builtin_amdgcn_sched_barrier(0);
             write_par(buf ^ 1, pa, pbd);
         }
-        const int rem = nw - nb * kAhead;
+        const int rem = nw - nb * kAh;
 #pragma unroll
-        for (int j = 0; j < kAhead - 1; ++j) {
+        for (int j = 0; j < kAh - 1; ++j) {
             if (j < rem) {
                 float an[N], bias, dskip;
                 read_par(nb & 1, j, an, bias, dskip);
@@ -397,7 +407,8 @@ __device__ __forceinline__ void record_call(const MeanStatus& st) {
 // groups workgroups of a chunk stores its channel group's sums (its waves
 // added in wave order) for k_mean_combine.
 template <int N, typename Tin, bool kTwoD, bool kRaw, bool kZoh>
-__global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
+__global__ __launch_bounds__(kC* kRedWaves)
+__attribute__((amdgpu_waves_per_eu(kZoh ? 1 : kWavesPaired))) void k_mean_reduce(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const float* __restrict__ D, const float* __restrict__ dt_bias,
     const Tin* __restrict__ xt, MeanWs ws, int K, int Dc, int L, int H, int W, int C, int nchunks,
@@ -405,8 +416,8 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_reduce(
     constexpr int kRows = part_rows<N, kRaw, kZoh>();
     __shared__ __align__(16) float part[kRedWaves][kRows][kC];
     record_call(st);
-    reduce_partials<N, Tin, kTwoD, kRaw, kZoh>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C,
-                                               softplus, groups);
+    reduce_partials<N, Tin, kTwoD, kRaw, kZoh, kZoh ? kAhead : kAheadPaired>(
+        part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, C, softplus, groups);
     __syncthreads();
     if (groups == 1) {
         scan_chunk<N, Tin, kRaw, kZoh>(part, Bm, ws, K, Dc, L, C, nchunks, blockIdx.x);
@@ -509,7 +520,8 @@ __device__ __forceinline__ void get_pair(float* p, float& a, float& b) {
 }
 
 template <int N, typename Tin, typename Tout, bool kTwoD, bool kRaw, bool kNt>
-__global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
+__global__ __launch_bounds__(kC* kRedWaves)
+__attribute__((amdgpu_waves_per_eu(kRaw ? 1 : kWavesPaired))) void k_mean_fused(
     const Tin* __restrict__ u, const Tin* __restrict__ delta, const float* __restrict__ A,
     const Tin* __restrict__ Bm, const Tin* __restrict__ Cm, const float* __restrict__ D,
     const float* __restrict__ dt_bias, const Tin* __restrict__ xt, MeanWs ws,
@@ -523,8 +535,8 @@ __global__ __launch_bounds__(kC* kRedWaves) void k_mean_fused(
     __shared__ int gave_up;
     const unsigned long long epoch = st.epoch;
     record_call(st);
-    reduce_partials<N, Tin, kTwoD, kRaw>(part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, kC,
-                                         softplus);
+    reduce_partials<N, Tin, kTwoD, kRaw, false, kRaw ? kAhead : kAheadPaired>(
+        part, u, delta, A, D, dt_bias, xt, K, Dc, L, H, W, kC, softplus);
     __syncthreads();
     const int chunk = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x % kC;
