@@ -6,7 +6,8 @@
 //   pi_0 = p, pi_1 = w*H + h, pi_2 = L-1-pi_0, pi_3 = L-1-pi_1.
 //
 // Planes that fit in LDS (the feature maps of VMamba's stages) are moved by
-// one workgroup each, 16 bytes per lane: directions 0 and 2 (and the merge's
+// one workgroup each (small planes, and for the cross-scan mid-size planes
+// when there are many, several to a workgroup), 16 bytes per lane: directions 0 and 2 (and the merge's
 // own row order) straight between registers and memory, directions 1 and 3
 // through a padded copy of the plane in LDS (row stride W + 1 words, so the
 // column walk is free of bank conflicts). Every global access is a full
@@ -287,16 +288,38 @@ inline int plane_tpp(int64_t H, int64_t W) {
     return H * (W + 1) <= kPlaneLdsWords / 12 ? 64 : kPlaneThreads;
 }
 
+// The cross-scan (and the column-major plane copies) also batch planes of up
+// to 4096 padded words, three per workgroup of 256 threads each, when there
+// are planes for at least four such workgroups per CU. A whole block on a
+// 56x56 bf16 plane leaves half its lanes idle (392 vectors of 8) and holds
+// two planes per CU, too few loads in flight: batch 128, 192 channels,
+// 139 -> 114 us. With few planes (stage-1, 192) batching would leave most CUs
+// idle. The merge keeps whole blocks: each of its planes already has four
+// inputs in flight, and three per workgroup took 250 against 223 us there.
+constexpr int64_t kBatchPlanesMin = 3 * 4 * 256;
+inline int scan_plane_tpp(int64_t planes, int64_t H, int64_t W) {
+    const int64_t words = H * (W + 1);
+    if (words > kPlaneLdsWords / 12 && words <= kPlaneLdsWords / 3 && planes >= kBatchPlanesMin)
+        return 256;
+    return plane_tpp(H, W);
+}
+
 template <typename T, int V, bool kAll>
 void launch_scan_tpp(const T* xi, T* xo, int64_t planes, int c, int h, int w, hipStream_t s) {
-    const int tpp = plane_tpp(h, w);
+    const int tpp = scan_plane_tpp(planes, h, w);
     const int ppw = kPlaneThreads / tpp;
     const dim3 grid(static_cast<unsigned>((planes + ppw - 1) / ppw)), block(kPlaneThreads);
     const int np = static_cast<int>(planes);
     // non-temporal stores for planes of whole cache lines (V > 1 only: others
     // are not)
     const bool nt = V > 1 && whole_lines(int64_t(h) * w, sizeof(T));
-    if (tpp == 64 && nt)
+    if (tpp == 256 && nt)
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 256, V != 1>), grid, block, 0, s, xi, xo,
+                           c, h, w, np);
+    else if (tpp == 256)
+        hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 256, false>), grid, block, 0, s, xi, xo,
+                           c, h, w, np);
+    else if (tpp == 64 && nt)
         hipLaunchKernelGGL((k_cross_scan_plane<T, V, kAll, 64, V != 1>), grid, block, 0, s, xi, xo, c,
                            h, w, np);
     else if (tpp == 64)

@@ -11,10 +11,12 @@ from paper_2412_16602_amd import vmb
 pytestmark = pytest.mark.gpu
 
 # whole-plane path (16-byte vectors, or single elements when L is not a
-# multiple of the vector) and 32 x 32 tiles for planes larger than LDS
+# multiple of the vector) and 32 x 32 tiles for planes larger than LDS; the
+# last two have enough mid-size planes for the cross-scan to take three per
+# workgroup (the second with a part-filled last workgroup and an odd L)
 SHAPES = [(1, 32, 7, 7), (2, 3, 56, 56), (1, 5, 1, 1), (1, 2, 1, 33), (2, 3, 33, 1),
           (1, 4, 40, 70), (3, 2, 64, 32), (1, 192, 56, 56), (1, 3, 6, 10), (1, 2, 128, 160),
-          (1, 2, 96, 127)]
+          (1, 2, 96, 127), (2, 1536, 40, 40), (1, 3073, 33, 35)]
 
 
 def _x(shape, seed, dtype):
